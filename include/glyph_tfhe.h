@@ -1,0 +1,208 @@
+/*
+ * glyph_tfhe.h -- C ABI of the MI355X TFHE activation library.
+ *
+ * Glyph (Lou, Feng, Fox, Jiang; arXiv 1911.07101) evaluates the nonlinear
+ * activations of encrypted DNN training with TFHE: a ReLU is one NOT without
+ * bootstrapping plus one bootstrapped AND per lower bit (Section 3.1,
+ * "Forward ReLU"), and table lookups are TFHE bootstraps (Section 3.1,
+ * "Forward Softmax"; functional bootstrapping in the cryptosystem switch,
+ * Section 3.2).  One gate bootstrap is: modulus switch of the LWE sample to
+ * Z_{2N}, blind rotation by n CMux external products (TRGSW key x TRLWE
+ * accumulator, gadget-decomposed, negacyclic in Z_{2^32}[X]/(X^N+1)),
+ * SampleExtract (Section 3.2, step 3) and LWE key switching (Section 3.2).
+ *
+ * Conventions (all calls):
+ *   - Torus elements are uint32_t; value x stands for x / 2^32; every torus
+ *     operation is mod 2^32.
+ *   - An LWE sample of dimension d is d+1 consecutive words [a_0 .. a_{d-1}, b];
+ *     a batch is row-major [count][d+1] with no padding.
+ *   - An encrypted bit is +1/8 (true) or -1/8 (false) on the torus.
+ *   - Every call returns 0 (TFHE_OK) or a negative TFHE_E* code;
+ *     tfhe_last_error() gives a message for the calling thread's last failure.
+ *   - "Client-side" calls (key generation, encryption, decryption, key export)
+ *     work on host memory and hold the secret key.  "Server-side" calls
+ *     (bootstraps, key switching, ReLU) take device pointers, enqueue work on
+ *     the given HIP stream (NULL = the legacy default stream) and return
+ *     without synchronising; they never allocate, copy to or from the host, or
+ *     read secret key material.
+ *   - Inputs and outputs of one server-side call must not overlap.  Concurrent
+ *     calls on different streams are safe when they use different workspaces.
+ */
+#ifndef GLYPH_TFHE_H
+#define GLYPH_TFHE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  TFHE_OK = 0,
+  TFHE_EINVAL = -1,       /* bad argument: NULL pointer, negative count, unknown gate,
+                             workspace too small, misaligned pointer */
+  TFHE_EUNSUPPORTED = -2, /* parameter set outside what the kernels are built for */
+  TFHE_ENOMEM = -3,       /* host or device allocation failed (key generation only) */
+  TFHE_EHIP = -4,         /* a HIP runtime call or kernel launch failed */
+  TFHE_EDEVICE = -5       /* the device is not a gfx950 GPU or does not exist */
+};
+
+/* TFHE parameters with k = 1 (one mask polynomial).
+ * Supported: N in {256, 512, 1024, 2048}; 1 <= n <= 4096; 2 <= bg_bit,
+ * l * bg_bit <= 32 and 2l * N * 2^(bg_bit-1) <= 2^22 (every coefficient of a
+ * product of digits by a 16-bit half of the key then stays within 2^37, which
+ * the NTT prime resolves exactly); ks_t * ks_basebit <= 32,
+ * 1 <= ks_basebit <= 8. */
+typedef struct {
+  int32_t n;          /* LWE dimension */
+  int32_t N;          /* TRLWE ring degree */
+  int32_t l;          /* bootstrapping-key gadget length */
+  int32_t bg_bit;     /* log2 of the gadget base */
+  int32_t ks_t;       /* key-switching digits */
+  int32_t ks_basebit; /* log2 of the key-switching base */
+  double alpha_lwe;   /* std. dev. of fresh-encryption noise (torus units) */
+  double alpha_bk;    /* std. dev. of bootstrapping-key noise */
+  double alpha_ks;    /* std. dev. of key-switching-key noise */
+} tfhe_params;
+
+typedef struct tfhe_secret_key tfhe_secret_key; /* host only: LWE key s, TRLWE key S */
+typedef struct tfhe_eval_key tfhe_eval_key;     /* device: bootstrapping + key-switching keys */
+
+/* two-input gates with bootstrapping (TFHE's gate set; the paper's ReLU uses
+ * ANDNY = AND(NOT a, b), Section 3.1) */
+enum tfhe_gate {
+  TFHE_NAND = 0, TFHE_AND = 1, TFHE_OR = 2, TFHE_NOR = 3, TFHE_XOR = 4, TFHE_XNOR = 5,
+  TFHE_ANDNY = 6, TFHE_ANDYN = 7, TFHE_ORNY = 8, TFHE_ORYN = 9
+};
+
+const char* tfhe_strerror(int rc);
+const char* tfhe_last_error(void);
+
+/* ---------------------------------------------------------------- keys ---- */
+
+/* Generate all keys deterministically from `seed` (Section 2: the user holds
+ * the private key, the server evaluates with public material only).
+ *   s (n bits), S (N bits): binary secret keys.
+ *   Bootstrapping key: n TRGSW samples of s_i under S, rows r = q*l + (j-1)
+ *     carrying s_i * 2^(32 - j*bg_bit) on polynomial q (0 = mask, 1 = body).
+ *   Key-switching key: LWE samples under s of v * S_i * 2^(32-(j+1)*basebit)
+ *     for i < N, j < ks_t, v in [1, 2^basebit).
+ * The evaluation key is uploaded to `device` (precomputed into the transform
+ * domain of the blind-rotation kernels); the secret key stays on the host.
+ * Both handles are owned by the caller and released with the *_free calls. */
+int tfhe_keygen_from_seed(const tfhe_params* params, uint64_t seed, int device,
+                          tfhe_secret_key** sk_out, tfhe_eval_key** ek_out);
+
+/* The two halves of tfhe_keygen_from_seed: the client-side key generation
+ * (host only, no device needed) and the upload of the evaluation key derived
+ * from it to `device`.  tfhe_keygen_from_seed(p, seed, dev, &sk, &ek) equals
+ * tfhe_secret_keygen(p, seed, &sk) followed by tfhe_eval_key_upload(sk, dev, &ek). */
+int tfhe_secret_keygen(const tfhe_params* params, uint64_t seed, tfhe_secret_key** sk_out);
+int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** ek_out);
+void tfhe_secret_key_free(tfhe_secret_key* sk);
+void tfhe_eval_key_free(tfhe_eval_key* ek);
+int tfhe_eval_key_params(const tfhe_eval_key* ek, tfhe_params* out);
+
+/* Copy keys out (host buffers; any pointer may be NULL to skip it).
+ *   s [n], S [N] (0/1 words); bk [n][2l][2][N] (coefficient domain);
+ *   ksk [N][ks_t][2^basebit - 1][n+1]. */
+int tfhe_export_keys(const tfhe_secret_key* sk, uint32_t* s, uint32_t* S, uint32_t* bk,
+                     uint32_t* ksk);
+
+/* --------------------------------------------------- client side (host) ---- */
+
+/* Fresh LWE encryptions under s of mu[0..count): ciphertext c is a pure
+ * function of (key, seed, first_index + c), so a large input can be produced
+ * in independent pieces.  ct: [count][n+1]. */
+int tfhe_encrypt_torus(const tfhe_secret_key* sk, uint64_t seed, const uint32_t* mu,
+                       int64_t first_index, int64_t count, uint32_t* ct);
+
+/* Decryption phase b - <a, key> of count samples.  key_kind 0: the LWE key s
+ * (samples of dimension n); 1: the TRLWE key S read as an LWE key of
+ * dimension N (samples produced by SampleExtract). */
+int tfhe_decrypt_phase(const tfhe_secret_key* sk, int key_kind, const uint32_t* ct,
+                       int64_t count, uint32_t* phase);
+
+/* Test polynomial of a table-lookup bootstrap over 2^msg_bits entries
+ * (message m encoded as m * 2^(31-msg_bits), one padding bit): coefficient j
+ * holds lut[floor((j + N/2^(msg_bits+1)) * 2^msg_bits / N)] * 2^(31-msg_bits)
+ * when that index is below 2^msg_bits, else -lut[0] * 2^(31-msg_bits).
+ * lut entries must be < 2^msg_bits; N >= 2^(msg_bits+1).  tv: [N] host. */
+int tfhe_lut_testvec(int32_t N, int32_t msg_bits, const uint32_t* lut, uint32_t* tv);
+
+/* ------------------------------------------------- server side (device) ---- */
+
+/* Device workspace in bytes that a bootstrap call over `batch` samples needs
+ * (256-byte aligned pointer required).  The workspace holds the modulus-
+ * switched inputs and the extracted samples between kernels. */
+int64_t tfhe_workspace_bytes(const tfhe_eval_key* ek, int64_t batch);
+
+/* Gate bootstrapping (Section 3.1, "TFHE homomorphic gates with
+ * bootstrapping"): out[c] = LWE_s(gate(ca[c], cb[c])) for c < B.
+ * ca, cb, out: [B][n+1] device.  The two inputs are combined linearly, the
+ * sum is bootstrapped with the constant test polynomial 1/8, extracted and
+ * key-switched back to dimension n.  B = 0 is a no-op. */
+int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca,
+                              const uint32_t* cb, uint32_t* out, int64_t B, void* workspace,
+                              int64_t workspace_bytes, void* stream);
+
+/* Table-lookup (programmable) bootstrap with key switching: out[c] encrypts
+ * the test polynomial's value selected by in[c]'s phase.  in, out: [B][n+1]
+ * device; testvec: [N] device (see tfhe_lut_testvec). */
+int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const uint32_t* testvec,
+                             uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes,
+                             void* stream);
+
+/* Blind rotation and SampleExtract without key switching: out[c] is an LWE
+ * sample of dimension N under S ([B][N+1] device).  testvec NULL selects the
+ * gate polynomial (1/8 everywhere).  Exposed so each stage can be checked. */
+int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in,
+                                 const uint32_t* testvec, uint32_t* out, int64_t B,
+                                 void* workspace, int64_t workspace_bytes, void* stream);
+
+/* LWE key switching (Section 3.2) from dimension N under S to dimension n
+ * under s: each a_i is rounded to ks_t*ks_basebit bits, split into ks_t
+ * digits (most significant first) and the key entries of the non-zero digits
+ * are subtracted from (0, b).  in: [B][N+1], out: [B][n+1], device. */
+int tfhe_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B,
+                         void* stream);
+
+/* Glyph forward ReLU unit (Section 3.1): x holds V encrypted values of
+ * `bits` two's-complement bits, LSB first, [V][bits][n+1] device.  Output bit
+ * i < bits-1 of value v is AND(NOT x[v][bits-1], x[v][i]) -- the NOT costs no
+ * bootstrap -- and output bit bits-1 is a trivial encryption of 0.
+ * Gate g of the whole tensor is bit g % (bits-1) of value g / (bits-1); a
+ * call computes gates [gate_begin, gate_end) (a streaming window) and writes
+ * the sign words of every value it touches.  y: [V][bits][n+1] device. */
+int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, int64_t V,
+                     int32_t bits, int64_t gate_begin, int64_t gate_end, void* workspace,
+                     int64_t workspace_bytes, void* stream);
+
+/* NOT without bootstrapping (Section 3.1): out = -in word by word.
+ * in, out: [count][dim+1] device. */
+int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);
+
+/* Exact negacyclic product in Z_{2^32}[X]/(X^N+1) of small signed digit
+ * polynomials by torus polynomials, computed by the same transform code as
+ * the blind rotation (digits in [-2^(bg-1), 2^(bg-1)) for the key's bg; the
+ * other factor is any uint32 polynomial).  d: [B][N] int32, b: [B][N],
+ * c: [B][N], device.  Exposed so the transform can be checked at extreme
+ * magnitudes against a schoolbook product. */
+int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
+                              uint32_t* c, int64_t B, void* stream);
+
+/* ---------------------------------------------------------- profiling ---- */
+
+/* Stage timing with HIP events.  While enabled (enable = 1), every server-side
+ * call records an event pair around each kernel it launches, on the call's
+ * stream.  tfhe_stage_times waits for the recorded events, returns the summed
+ * milliseconds and launch counts of the three stages -- index 0: input
+ * combination and modulus switch, 1: blind rotation with SampleExtract,
+ * 2: key switching -- and clears the record.  enable = 0 stops recording.
+ * Host-side state, shared by all threads; not for use during graph capture. */
+int tfhe_stage_timing(int enable);
+int tfhe_stage_times(double* ms /*[3]*/, int64_t* launches /*[3]*/);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

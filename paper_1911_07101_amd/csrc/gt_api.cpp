@@ -1,0 +1,469 @@
+// C ABI of the library (declared in include/glyph_tfhe.h): argument checks,
+// key handles, workspace carving and kernel launches.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "gt_internal.h"
+
+namespace gt {
+
+namespace {
+thread_local char g_msg[512] = "";
+}
+
+int fail(int rc, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_msg, sizeof(g_msg), fmt, ap);
+  va_end(ap);
+  return rc;
+}
+
+int check_params(const tfhe_params& p) {
+  if (p.N != 256 && p.N != 512 && p.N != 1024 && p.N != 2048)
+    return fail(TFHE_EUNSUPPORTED, "N=%d: supported ring degrees are 256, 512, 1024, 2048", p.N);
+  if (p.n < 1 || p.n > 4096) return fail(TFHE_EUNSUPPORTED, "n=%d outside [1, 4096]", p.n);
+  if (p.l < 1 || p.bg_bit < 2 || p.l * p.bg_bit > 32)
+    return fail(TFHE_EUNSUPPORTED, "gadget l=%d bg_bit=%d: need bg_bit >= 2 and l*bg_bit <= 32", p.l,
+                p.bg_bit);
+  // every coefficient of sum_r digit_r * half_r must stay within 2^37 < P/2 - 2^37
+  const double bound = 2.0 * p.l * p.N * static_cast<double>(1u << (p.bg_bit - 1));
+  if (bound > 4194304.0)
+    return fail(TFHE_EUNSUPPORTED, "2l*N*Bg/2 = %.0f exceeds 2^22 (exactness bound of the transform)", bound);
+  if (p.ks_basebit < 1 || p.ks_basebit > 8 || p.ks_t < 1 || p.ks_t * p.ks_basebit > 32)
+    return fail(TFHE_EUNSUPPORTED, "key switching t=%d basebit=%d: need 1<=basebit<=8, t*basebit<=32",
+                p.ks_t, p.ks_basebit);
+  if (!(p.alpha_lwe >= 0.0) || !(p.alpha_bk >= 0.0) || !(p.alpha_ks >= 0.0))
+    return fail(TFHE_EINVAL, "noise parameters must be >= 0");
+  return TFHE_OK;
+}
+
+}  // namespace gt
+
+using namespace gt;
+
+namespace {
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(TFHE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// make the eval key's device current for the duration of a call
+struct DeviceGuard {
+  int prev = -1;
+  bool ok = true;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) != hipSuccess) prev = -1;
+    if (prev != dev) ok = hipSetDevice(dev) == hipSuccess;
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+int check_ws(const tfhe_eval_key* ek, void* ws, int64_t ws_bytes, int64_t B) {
+  if (ws == nullptr) return fail(TFHE_EINVAL, "workspace is NULL");
+  if (!aligned(ws, 256)) return fail(TFHE_EINVAL, "workspace must be 256-byte aligned");
+  const int64_t need = workspace_bytes(ek->p, B);
+  if (ws_bytes < need)
+    return fail(TFHE_EINVAL, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                static_cast<long long>(ws_bytes), static_cast<long long>(need));
+  return TFHE_OK;
+}
+
+struct PhaseCtx {
+  const std::vector<uint32_t>* key;
+  const uint32_t* ct;
+  uint32_t* phase;
+};
+
+void phase_rows(int64_t begin, int64_t end, void* vctx) {
+  const PhaseCtx& c = *static_cast<PhaseCtx*>(vctx);
+  const int64_t dim = static_cast<int64_t>(c.key->size());
+  const uint32_t* key = c.key->data();
+  for (int64_t k = begin; k < end; k++) {
+    const uint32_t* x = c.ct + k * (dim + 1);
+    uint32_t v = x[dim];
+    for (int64_t m = 0; m < dim; m++) v -= x[m] * key[m];
+    c.phase[k] = v;
+  }
+}
+
+// ---- stage timing (event pairs recorded around each launch while enabled)
+struct StageEvent {
+  int stage;
+  hipEvent_t start, stop;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<StageEvent> g_prof_events;
+
+struct StageScope {
+  StageEvent ev{};
+  bool on = false;
+  hipStream_t st;
+  StageScope(int stage, void* stream) : st(static_cast<hipStream_t>(stream)) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof_on) return;
+    ev.stage = stage;
+    if (hipEventCreate(&ev.start) != hipSuccess) return;
+    if (hipEventCreate(&ev.stop) != hipSuccess) {
+      (void)hipEventDestroy(ev.start);
+      return;
+    }
+    on = hipEventRecord(ev.start, st) == hipSuccess;
+  }
+  ~StageScope() {
+    if (!on) return;
+    (void)hipEventRecord(ev.stop, st);
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    g_prof_events.push_back(ev);
+  }
+};
+
+int check_u32(const void* p, const char* name) {
+  if (p == nullptr) return fail(TFHE_EINVAL, "%s is NULL", name);
+  if (!aligned(p, 4)) return fail(TFHE_EINVAL, "%s is not 4-byte aligned", name);
+  return TFHE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tfhe_strerror(int rc) {
+  switch (rc) {
+    case TFHE_OK: return "ok";
+    case TFHE_EINVAL: return "invalid argument";
+    case TFHE_EUNSUPPORTED: return "unsupported parameters";
+    case TFHE_ENOMEM: return "out of memory";
+    case TFHE_EHIP: return "HIP runtime error";
+    case TFHE_EDEVICE: return "no usable gfx950 device";
+    default: return "unknown error";
+  }
+}
+
+const char* tfhe_last_error(void) { return g_msg; }
+
+int tfhe_secret_keygen(const tfhe_params* params, uint64_t seed, tfhe_secret_key** sk_out) {
+  if (params == nullptr || sk_out == nullptr) return fail(TFHE_EINVAL, "NULL argument to tfhe_secret_keygen");
+  *sk_out = nullptr;
+  int rc = check_params(*params);
+  if (rc) return rc;
+  tfhe_secret_key* sk = new (std::nothrow) tfhe_secret_key();
+  if (!sk) return fail(TFHE_ENOMEM, "host allocation failed");
+  sk->p = *params;
+  sk->seed = seed;
+  try {
+    keygen_host(*sk);
+  } catch (const std::bad_alloc&) {
+    delete sk;
+    return fail(TFHE_ENOMEM, "host allocation failed during key generation");
+  }
+  *sk_out = sk;
+  return TFHE_OK;
+}
+
+int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** ek_out) {
+  if (sk == nullptr || ek_out == nullptr) return fail(TFHE_EINVAL, "NULL argument to tfhe_eval_key_upload");
+  *ek_out = nullptr;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev)
+    return fail(TFHE_EDEVICE, "device %d does not exist (%d visible)", device, ndev);
+  hipDeviceProp_t prop;
+  if (hipGetDeviceProperties(&prop, device) != hipSuccess) return fail(TFHE_EDEVICE, "cannot query device %d", device);
+  if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+    return fail(TFHE_EDEVICE, "device %d is %s; the kernels are built for gfx950", device, prop.gcnArchName);
+
+  const tfhe_params& p = sk->p;
+  tfhe_eval_key* ek = new (std::nothrow) tfhe_eval_key();
+  if (!ek) return fail(TFHE_ENOMEM, "host allocation failed");
+  ek->p = p;
+  ek->device = device;
+  ek->bk_ntt = nullptr;
+  ek->tw_fwd = ek->tw_inv = nullptr;
+  ek->ksk = nullptr;
+  ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 4 * p.N * 8;
+  ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
+
+  std::vector<double> bk_host, tw(2 * static_cast<size_t>(p.N));
+  try {
+    bk_host.resize(static_cast<size_t>(ek->bk_bytes / 8));
+  } catch (const std::bad_alloc&) {
+    delete ek;
+    return fail(TFHE_ENOMEM, "host allocation failed for the transform-domain key");
+  }
+  bk_to_transform_host(p, sk->bk.data(), bk_host.data());
+  twiddles_host(p.N, tw.data(), tw.data() + p.N);
+
+  int rc = TFHE_OK;
+  hipError_t e;
+  DeviceGuard g(device);
+  if (!g.ok) {
+    rc = fail(TFHE_EDEVICE, "cannot select device %d", device);
+    goto fail_out;
+  }
+  if ((e = hipMalloc(&ek->bk_ntt, ek->bk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(bk): %s", hipGetErrorString(e)); goto fail_out; }
+  if ((e = hipMalloc(&ek->tw_fwd, 2 * sizeof(double) * p.N)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(twiddles): %s", hipGetErrorString(e)); goto fail_out; }
+  ek->tw_inv = ek->tw_fwd + p.N;
+  if ((e = hipMalloc(&ek->ksk, ek->ksk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(ksk): %s", hipGetErrorString(e)); goto fail_out; }
+  if ((e = hipMemcpy(ek->bk_ntt, bk_host.data(), ek->bk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy bk"); goto fail_out; }
+  if ((e = hipMemcpy(ek->tw_fwd, tw.data(), 2 * sizeof(double) * p.N, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy twiddles"); goto fail_out; }
+  if ((e = hipMemcpy(ek->ksk, sk->ksk.data(), ek->ksk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy ksk"); goto fail_out; }
+  *ek_out = ek;
+  return TFHE_OK;
+
+fail_out:
+  tfhe_eval_key_free(ek);
+  return rc;
+}
+
+int tfhe_keygen_from_seed(const tfhe_params* params, uint64_t seed, int device,
+                          tfhe_secret_key** sk_out, tfhe_eval_key** ek_out) {
+  if (params == nullptr || sk_out == nullptr || ek_out == nullptr)
+    return fail(TFHE_EINVAL, "NULL argument to tfhe_keygen_from_seed");
+  *sk_out = nullptr;
+  *ek_out = nullptr;
+  tfhe_secret_key* sk = nullptr;
+  int rc = tfhe_secret_keygen(params, seed, &sk);
+  if (rc) return rc;
+  rc = tfhe_eval_key_upload(sk, device, ek_out);
+  if (rc) {
+    delete sk;
+    return rc;
+  }
+  *sk_out = sk;
+  return TFHE_OK;
+}
+
+void tfhe_secret_key_free(tfhe_secret_key* sk) { delete sk; }
+
+void tfhe_eval_key_free(tfhe_eval_key* ek) {
+  if (!ek) return;
+  DeviceGuard g(ek->device);
+  if (ek->bk_ntt) (void)hipFree(ek->bk_ntt);
+  if (ek->tw_fwd) (void)hipFree(ek->tw_fwd);
+  if (ek->ksk) (void)hipFree(ek->ksk);
+  delete ek;
+}
+
+int tfhe_eval_key_params(const tfhe_eval_key* ek, tfhe_params* out) {
+  if (!ek || !out) return fail(TFHE_EINVAL, "NULL argument");
+  *out = ek->p;
+  return TFHE_OK;
+}
+
+int tfhe_export_keys(const tfhe_secret_key* sk, uint32_t* s, uint32_t* S, uint32_t* bk, uint32_t* ksk) {
+  if (!sk) return fail(TFHE_EINVAL, "NULL secret key");
+  if (s) std::memcpy(s, sk->s.data(), sk->s.size() * 4);
+  if (S) std::memcpy(S, sk->S.data(), sk->S.size() * 4);
+  if (bk) std::memcpy(bk, sk->bk.data(), sk->bk.size() * 4);
+  if (ksk) std::memcpy(ksk, sk->ksk.data(), sk->ksk.size() * 4);
+  return TFHE_OK;
+}
+
+int tfhe_encrypt_torus(const tfhe_secret_key* sk, uint64_t seed, const uint32_t* mu, int64_t first_index,
+                       int64_t count, uint32_t* ct) {
+  if (!sk) return fail(TFHE_EINVAL, "NULL secret key");
+  if (count < 0 || first_index < 0) return fail(TFHE_EINVAL, "negative count or index");
+  if (count == 0) return TFHE_OK;
+  if (!mu || !ct) return fail(TFHE_EINVAL, "NULL buffer");
+  encrypt_host(*sk, seed, mu, first_index, count, ct);
+  return TFHE_OK;
+}
+
+int tfhe_decrypt_phase(const tfhe_secret_key* sk, int key_kind, const uint32_t* ct, int64_t count,
+                       uint32_t* phase) {
+  if (!sk) return fail(TFHE_EINVAL, "NULL secret key");
+  if (key_kind != 0 && key_kind != 1) return fail(TFHE_EINVAL, "key_kind must be 0 or 1");
+  if (count < 0) return fail(TFHE_EINVAL, "negative count");
+  if (count == 0) return TFHE_OK;
+  if (!ct || !phase) return fail(TFHE_EINVAL, "NULL buffer");
+  PhaseCtx ctx{key_kind == 0 ? &sk->s : &sk->S, ct, phase};
+  parallel_for(count, 4096, phase_rows, &ctx);
+  return TFHE_OK;
+}
+
+int tfhe_lut_testvec(int32_t N, int32_t msg_bits, const uint32_t* lut, uint32_t* tv) {
+  if (!lut || !tv) return fail(TFHE_EINVAL, "NULL buffer");
+  if (msg_bits < 1 || msg_bits > 30 || N < (2 << msg_bits) || (N & (N - 1)) != 0)
+    return fail(TFHE_EINVAL, "need N a power of two with N >= 2^(msg_bits+1), 1 <= msg_bits <= 30");
+  const int64_t M = int64_t{1} << msg_bits;
+  const int shift = 31 - msg_bits;
+  for (int64_t k = 0; k < M; k++)
+    if (lut[k] >= static_cast<uint32_t>(M)) return fail(TFHE_EINVAL, "lut[%lld] = %u is not below 2^%d",
+                                                         static_cast<long long>(k), lut[k], msg_bits);
+  const int64_t box = N / M;  // coefficients per table entry
+  for (int32_t j = 0; j < N; j++) {
+    const int64_t idx = (j + box / 2) / box;
+    tv[j] = idx < M ? lut[idx] << shift : 0u - (lut[0] << shift);
+  }
+  return TFHE_OK;
+}
+
+int64_t tfhe_workspace_bytes(const tfhe_eval_key* ek, int64_t batch) {
+  if (!ek || batch < 0) return fail(TFHE_EINVAL, "bad argument to tfhe_workspace_bytes");
+  return workspace_bytes(ek->p, batch);
+}
+
+static int bootstrap_common(const tfhe_eval_key* ek, const PrepArgs& a, const uint32_t* testvec,
+                            uint32_t* out, int out_mode, void* ws, int64_t ws_bytes, void* stream,
+                            bool keyswitch) {
+  int rc = check_ws(ek, ws, ws_bytes, a.B);
+  if (rc) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  Workspace w = carve_workspace(ek->p, ws, a.B);
+  {
+    StageScope sc(0, stream);
+    if ((rc = launch_prep(ek, a, w, stream))) return rc;
+  }
+  {
+    StageScope sc(1, stream);
+    if ((rc = launch_blind_rotate(ek, w, testvec, a.B, stream))) return rc;
+  }
+  if (!keyswitch) {
+    hipError_t e = hipMemcpyAsync(out, w.extract, static_cast<size_t>(a.B) * (ek->p.N + 1) * 4,
+                                  hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? TFHE_OK : hip_fail(e, "copy extracted samples");
+  }
+  StageScope sc(2, stream);
+  return launch_keyswitch(ek, w.extract, out, a.B, out_mode, a.bits, a.gate_begin, stream);
+}
+
+int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
+                              uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_,
+                              void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (gate < TFHE_NAND || gate > TFHE_ORYN) return fail(TFHE_EINVAL, "unknown gate %d", gate);
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(ca, "ca")) || (rc = check_u32(cb, "cb")) || (rc = check_u32(out, "out"))) return rc;
+  PrepArgs a{kModeGate, gate, ca, cb, B, 0, 0};
+  return bootstrap_common(ek, a, nullptr, out, kModeGate, workspace, workspace_bytes_, stream, true);
+}
+
+int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const uint32_t* testvec,
+                             uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_,
+                             void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(in, "in")) || (rc = check_u32(testvec, "testvec")) || (rc = check_u32(out, "out")))
+    return rc;
+  PrepArgs a{kModePlain, 0, in, nullptr, B, 0, 0};
+  return bootstrap_common(ek, a, testvec, out, kModePlain, workspace, workspace_bytes_, stream, true);
+}
+
+int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in, const uint32_t* testvec,
+                                 uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_,
+                                 void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
+  if (testvec && !aligned(testvec, 4)) return fail(TFHE_EINVAL, "testvec is not 4-byte aligned");
+  PrepArgs a{kModePlain, 0, in, nullptr, B, 0, 0};
+  return bootstrap_common(ek, a, testvec, out, kModePlain, workspace, workspace_bytes_, stream, false);
+}
+
+int tfhe_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  StageScope sc(2, stream);
+  return launch_keyswitch(ek, in, out, B, kModePlain, 0, 0, stream);
+}
+
+int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, int64_t V, int32_t bits,
+                     int64_t gate_begin, int64_t gate_end, void* workspace, int64_t workspace_bytes_,
+                     void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (V < 0 || bits < 2 || bits > 64) return fail(TFHE_EINVAL, "need V >= 0 and 2 <= bits <= 64");
+  const int64_t total = V * (bits - 1);
+  if (gate_begin < 0 || gate_end < gate_begin || gate_end > total)
+    return fail(TFHE_EINVAL, "gate window [%lld, %lld) outside [0, %lld)", static_cast<long long>(gate_begin),
+                static_cast<long long>(gate_end), static_cast<long long>(total));
+  const int64_t B = gate_end - gate_begin;
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(x, "x")) || (rc = check_u32(y, "y"))) return rc;
+  PrepArgs a{kModeRelu, TFHE_ANDNY, x, nullptr, B, bits, gate_begin};
+  rc = bootstrap_common(ek, a, nullptr, y, kModeRelu, workspace, workspace_bytes_, stream, true);
+  if (rc) return rc;
+  const int64_t v_begin = gate_begin / (bits - 1);
+  const int64_t v_end = (gate_end - 1) / (bits - 1) + 1;
+  DeviceGuard g(ek->device);
+  return launch_relu_sign(ek, y, bits, v_begin, v_end, stream);
+}
+
+int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {
+  if (dim < 1 || count < 0) return fail(TFHE_EINVAL, "need dim >= 1 and count >= 0");
+  if (count == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
+  return launch_not(dim, in, out, count, stream);
+}
+
+int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c,
+                              int64_t B, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(d, "d")) || (rc = check_u32(b, "b")) || (rc = check_u32(c, "c"))) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  return launch_negacyclic_mul(ek, d, b, c, B, stream);
+}
+
+int tfhe_stage_timing(int enable) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = enable != 0;
+  return TFHE_OK;
+}
+
+int tfhe_stage_times(double* ms, int64_t* launches) {
+  if (!ms || !launches) return fail(TFHE_EINVAL, "NULL argument");
+  std::vector<StageEvent> evs;
+  {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    evs.swap(g_prof_events);
+  }
+  for (int k = 0; k < 3; k++) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  int rc = TFHE_OK;
+  for (auto& ev : evs) {
+    float t = 0.f;
+    hipError_t e = hipEventSynchronize(ev.stop);
+    if (e == hipSuccess) e = hipEventElapsedTime(&t, ev.start, ev.stop);
+    if (e != hipSuccess && rc == TFHE_OK) rc = hip_fail(e, "stage event");
+    if (e == hipSuccess && ev.stage >= 0 && ev.stage < 3) {
+      ms[ev.stage] += t;
+      launches[ev.stage] += 1;
+    }
+    (void)hipEventDestroy(ev.start);
+    (void)hipEventDestroy(ev.stop);
+  }
+  return rc;
+}
+
+}  // extern "C"

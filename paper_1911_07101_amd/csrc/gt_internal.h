@@ -1,0 +1,82 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "glyph_tfhe.h"
+
+struct tfhe_secret_key {
+  tfhe_params p;
+  uint64_t seed;
+  std::vector<uint32_t> s;    // [n] 0/1
+  std::vector<uint32_t> S;    // [N] 0/1
+  std::vector<uint32_t> bk;   // [n][2l][2][N] coefficient domain
+  std::vector<uint32_t> ksk;  // [N][t][base-1][n+1]
+};
+
+struct tfhe_eval_key {
+  tfhe_params p;
+  int device;
+  double* bk_ntt;   // device [n][2l][4][N] in transform-domain layout, times N^-1
+  double* tw_fwd;   // device [N]: psi^brv(k)
+  double* tw_inv;   // device [N]: psi^-brv(k)
+  uint32_t* ksk;    // device [N][t][base-1][n+1]
+  int64_t bk_bytes;
+  int64_t ksk_bytes;
+};
+
+namespace gt {
+
+// error reporting (thread-local message)
+int fail(int rc, const char* fmt, ...);
+int check_params(const tfhe_params& p);
+
+// generator tags
+enum : uint32_t {
+  kTagLweKey = 1, kTagRlweKey = 2, kTagBkMask = 3, kTagBkNoise = 4,
+  kTagKskMask = 5, kTagKskNoise = 6, kTagEncMask = 7, kTagEncNoise = 8
+};
+
+// host-side cryptography (gt_host.cpp)
+uint64_t rand_word(uint64_t seed, uint32_t tag, uint64_t idx);
+uint32_t rand_noise(uint64_t seed, uint32_t tag, uint64_t idx, double alpha);
+void keygen_host(tfhe_secret_key& sk);
+void encrypt_host(const tfhe_secret_key& sk, uint64_t seed, const uint32_t* mu, int64_t first,
+                  int64_t count, uint32_t* ct);
+void bk_to_transform_host(const tfhe_params& p, const uint32_t* bk, double* out);
+void twiddles_host(int N, double* fwd, double* inv);
+void parallel_for(int64_t count, int64_t grain, void (*fn)(int64_t, int64_t, void*), void* ctx);
+
+// device launchers (gt_kernels.hip); return TFHE_OK or TFHE_EHIP
+struct Workspace {
+  uint16_t* abar;     // [B][n+1] modulus-switched inputs
+  uint32_t* extract;  // [B][N+1] extracted samples
+};
+int64_t workspace_bytes(const tfhe_params& p, int64_t B);
+Workspace carve_workspace(const tfhe_params& p, void* ws, int64_t B);
+
+enum InputMode : int { kModeGate = 0, kModePlain = 1, kModeRelu = 2 };
+
+struct PrepArgs {
+  int mode;
+  int gate;
+  const uint32_t* ca;  // gate: first operand; plain: the input; relu: x
+  const uint32_t* cb;  // gate: second operand
+  int64_t B;
+  int32_t bits;        // relu
+  int64_t gate_begin;  // relu
+};
+
+int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws, void* stream);
+int launch_blind_rotate(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec,
+                        int64_t B, void* stream);
+int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B,
+                     int mode, int32_t bits, int64_t gate_begin, void* stream);
+int launch_relu_sign(const tfhe_eval_key* ek, uint32_t* y, int32_t bits, int64_t v_begin,
+                     int64_t v_end, void* stream);
+int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);
+int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
+                          uint32_t* c, int64_t B, void* stream);
+
+}  // namespace gt

@@ -1,0 +1,334 @@
+"""Python binding of libglyph_tfhe.so (include/glyph_tfhe.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  Device buffers are torch tensors on a ROCm device (int32 tensors
+hold the raw uint32 torus words); streams are torch streams.  Host buffers are
+numpy uint32 arrays.  The functions carry the C names.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libglyph_tfhe.so")
+
+TFHE_OK, TFHE_EINVAL, TFHE_EUNSUPPORTED, TFHE_ENOMEM, TFHE_EHIP, TFHE_EDEVICE = 0, -1, -2, -3, -4, -5
+GATES = {"NAND": 0, "AND": 1, "OR": 2, "NOR": 3, "XOR": 4, "XNOR": 5,
+         "ANDNY": 6, "ANDYN": 7, "ORNY": 8, "ORYN": 9}
+MU = 1 << 29
+
+
+class TfheError(RuntimeError):
+    def __init__(self, rc: int, msg: str):
+        super().__init__(f"{msg} (rc={rc})")
+        self.rc = rc
+
+
+class tfhe_params(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("N", ctypes.c_int32), ("l", ctypes.c_int32),
+                ("bg_bit", ctypes.c_int32), ("ks_t", ctypes.c_int32),
+                ("ks_basebit", ctypes.c_int32), ("alpha_lwe", ctypes.c_double),
+                ("alpha_bk", ctypes.c_double), ("alpha_ks", ctypes.c_double)]
+
+
+def make_params(d) -> tfhe_params:
+    if isinstance(d, tfhe_params):
+        return d
+    return tfhe_params(d["n"], d["N"], d["l"], d["bg_bit"], d["ks_t"], d["ks_basebit"],
+                       d["alpha_lwe"], d["alpha_bk"], d.get("alpha_ks", d["alpha_lwe"]))
+
+
+_lib = None
+_vp = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+_u64 = ctypes.c_uint64
+
+_SIGNATURES = {
+    "tfhe_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "tfhe_last_error": (ctypes.c_char_p, []),
+    "tfhe_keygen_from_seed": (ctypes.c_int, [_vp, _u64, ctypes.c_int, _vp, _vp]),
+    "tfhe_secret_keygen": (ctypes.c_int, [_vp, _u64, _vp]),
+    "tfhe_eval_key_upload": (ctypes.c_int, [_vp, ctypes.c_int, _vp]),
+    "tfhe_secret_key_free": (None, [_vp]),
+    "tfhe_eval_key_free": (None, [_vp]),
+    "tfhe_eval_key_params": (ctypes.c_int, [_vp, _vp]),
+    "tfhe_export_keys": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp]),
+    "tfhe_encrypt_torus": (ctypes.c_int, [_vp, _u64, _vp, _i64, _i64, _vp]),
+    "tfhe_decrypt_phase": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _i64, _vp]),
+    "tfhe_lut_testvec": (ctypes.c_int, [_i32, _i32, _vp, _vp]),
+    "tfhe_workspace_bytes": (_i64, [_vp, _i64]),
+    "tfhe_gate_bootstrap_batch": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
+    "tfhe_lut_bootstrap_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
+    "tfhe_bootstrap_extract_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
+    "tfhe_keyswitch_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp]),
+    "glyph_relu_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
+    "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
+    "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
+    "tfhe_stage_timing": (ctypes.c_int, [ctypes.c_int]),
+    "tfhe_stage_times": (ctypes.c_int, [_vp, _vp]),
+}
+
+
+def lib():
+    """The loaded library.  Raises if it has not been built: there is no
+    fallback path."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != TFHE_OK:
+        raise TfheError(rc, lib().tfhe_last_error().decode() or lib().tfhe_strerror(rc).decode())
+
+
+def _host_u32(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint32:
+        a = a.astype(np.uint32)
+    return a
+
+
+def _hptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _dptr(t):
+    """Device pointer of a torch tensor (must be contiguous and on a GPU)."""
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+# ---------------------------------------------------------------- keys
+
+class SecretKey:
+    def __init__(self, handle, params: tfhe_params):
+        self._h = handle
+        self.params = params
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.tfhe_secret_key_free(self._h)
+            self._h = None
+
+
+class EvalKey:
+    def __init__(self, handle, params: tfhe_params, device: int):
+        self._h = handle
+        self.params = params
+        self.device = device
+
+    @property
+    def handle(self):
+        return self._h
+
+    def free(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.tfhe_eval_key_free(self._h)
+            self._h = None
+
+    def __del__(self):
+        self.free()
+
+
+def tfhe_secret_keygen(params, seed: int) -> SecretKey:
+    p = make_params(params)
+    h = ctypes.c_void_p()
+    _check(lib().tfhe_secret_keygen(ctypes.byref(p), seed, ctypes.byref(h)))
+    return SecretKey(h, p)
+
+
+def tfhe_eval_key_upload(sk: SecretKey, device: int = 0) -> EvalKey:
+    h = ctypes.c_void_p()
+    _check(lib().tfhe_eval_key_upload(sk.handle, device, ctypes.byref(h)))
+    return EvalKey(h, sk.params, device)
+
+
+def tfhe_keygen_from_seed(params, seed: int, device: int = 0):
+    p = make_params(params)
+    hs, he = ctypes.c_void_p(), ctypes.c_void_p()
+    _check(lib().tfhe_keygen_from_seed(ctypes.byref(p), seed, device, ctypes.byref(hs), ctypes.byref(he)))
+    return SecretKey(hs, p), EvalKey(he, p, device)
+
+
+def tfhe_export_keys(sk: SecretKey) -> dict:
+    p = sk.params
+    base = (1 << p.ks_basebit) - 1
+    s = np.zeros(p.n, np.uint32)
+    S = np.zeros(p.N, np.uint32)
+    bk = np.zeros(p.n * 2 * p.l * 2 * p.N, np.uint32)
+    ksk = np.zeros(p.N * p.ks_t * base * (p.n + 1), np.uint32)
+    _check(lib().tfhe_export_keys(sk.handle, _hptr(s), _hptr(S), _hptr(bk), _hptr(ksk)))
+    return {"s": s, "S": S, "bk": bk, "ksk": ksk}
+
+
+# ---------------------------------------------------------- client side
+
+def tfhe_encrypt_torus(sk: SecretKey, seed: int, mu, first_index: int = 0) -> np.ndarray:
+    mu = _host_u32(mu).ravel()
+    ct = np.zeros((len(mu), sk.params.n + 1), np.uint32)
+    _check(lib().tfhe_encrypt_torus(sk.handle, seed, _hptr(mu), first_index, len(mu), _hptr(ct)))
+    return ct
+
+
+def tfhe_decrypt_phase(sk: SecretKey, ct, key_kind: int = 0) -> np.ndarray:
+    ct = _host_u32(ct)
+    dim = ct.shape[-1] - 1
+    count = ct.size // (dim + 1)
+    out = np.zeros(count, np.uint32)
+    _check(lib().tfhe_decrypt_phase(sk.handle, key_kind, _hptr(ct), count, _hptr(out)))
+    return out.reshape(ct.shape[:-1])
+
+
+def tfhe_lut_testvec(N: int, msg_bits: int, lut) -> np.ndarray:
+    lut = _host_u32(lut)
+    tv = np.zeros(N, np.uint32)
+    _check(lib().tfhe_lut_testvec(N, msg_bits, _hptr(lut), _hptr(tv)))
+    return tv
+
+
+def encode_bits(bits) -> np.ndarray:
+    """+1/8 for true, -1/8 for false."""
+    b = np.asarray(bits).astype(np.int64)
+    return np.where(b != 0, MU, (1 << 32) - MU).astype(np.uint32)
+
+
+# ---------------------------------------------------------- server side
+
+def to_device(a: np.ndarray, device: int = 0):
+    import torch
+    a = _host_u32(a)
+    return torch.from_numpy(a.view(np.int32)).to(f"cuda:{device}")
+
+
+def to_host(t) -> np.ndarray:
+    return t.detach().cpu().numpy().view(np.uint32)
+
+
+def tfhe_workspace_bytes(ek: EvalKey, batch: int) -> int:
+    v = lib().tfhe_workspace_bytes(ek.handle, batch)
+    if v < 0:
+        _check(int(v))
+    return int(v)
+
+
+def alloc_workspace(ek: EvalKey, batch: int):
+    import torch
+    return torch.empty(max(tfhe_workspace_bytes(ek, batch), 256), dtype=torch.uint8,
+                       device=f"cuda:{ek.device}")
+
+
+def _empty(shape, ek: EvalKey):
+    import torch
+    return torch.empty(shape, dtype=torch.int32, device=f"cuda:{ek.device}")
+
+
+def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=None, stream=None):
+    B = ca.shape[0]
+    n = ek.params.n
+    out = _empty((B, n + 1), ek) if out is None else out
+    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    g = GATES[gate] if isinstance(gate, str) else int(gate)
+    _check(lib().tfhe_gate_bootstrap_batch(ek.handle, g, _dptr(ca), _dptr(cb), _dptr(out), B,
+                                           _dptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def tfhe_lut_bootstrap_batch(ek: EvalKey, x, testvec, out=None, workspace=None, stream=None):
+    B = x.shape[0]
+    out = _empty((B, ek.params.n + 1), ek) if out is None else out
+    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    _check(lib().tfhe_lut_bootstrap_batch(ek.handle, _dptr(x), _dptr(testvec), _dptr(out), B,
+                                          _dptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def tfhe_bootstrap_extract_batch(ek: EvalKey, x, testvec=None, out=None, workspace=None, stream=None):
+    B = x.shape[0]
+    out = _empty((B, ek.params.N + 1), ek) if out is None else out
+    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    tv = _dptr(testvec) if testvec is not None else ctypes.c_void_p(0)
+    _check(lib().tfhe_bootstrap_extract_batch(ek.handle, _dptr(x), tv, _dptr(out), B, _dptr(ws),
+                                              ws.numel(), _stream(stream)))
+    return out
+
+
+def tfhe_keyswitch_batch(ek: EvalKey, x, out=None, stream=None):
+    B = x.shape[0]
+    out = _empty((B, ek.params.n + 1), ek) if out is None else out
+    _check(lib().tfhe_keyswitch_batch(ek.handle, _dptr(x), _dptr(out), B, _stream(stream)))
+    return out
+
+
+def glyph_relu_batch(ek: EvalKey, x, bits: int, y=None, gate_begin: int = 0, gate_end=None,
+                     workspace=None, stream=None):
+    V = x.shape[0]
+    n = ek.params.n
+    y = _empty((V, bits, n + 1), ek) if y is None else y
+    if gate_end is None:
+        gate_end = V * (bits - 1)
+    ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
+    _check(lib().glyph_relu_batch(ek.handle, _dptr(x), _dptr(y), V, bits, gate_begin, gate_end,
+                                  _dptr(ws), ws.numel(), _stream(stream)))
+    return y
+
+
+def tfhe_not_batch(x, out=None, stream=None):
+    import torch
+    dim = x.shape[-1] - 1
+    count = x.numel() // (dim + 1)
+    out = torch.empty_like(x) if out is None else out
+    _check(lib().tfhe_not_batch(dim, _dptr(x), _dptr(out), count, _stream(stream)))
+    return out
+
+
+def tfhe_negacyclic_mul_batch(ek: EvalKey, d, b, out=None, stream=None):
+    import torch
+    B = d.shape[0]
+    out = torch.empty_like(b) if out is None else out
+    _check(lib().tfhe_negacyclic_mul_batch(ek.handle, _dptr(d), _dptr(b), _dptr(out), B,
+                                           _stream(stream)))
+    return out
+
+
+# ---------------------------------------------------------------- profiling
+
+STAGES = ("prep", "blind_rotate", "keyswitch")
+
+
+def tfhe_stage_timing(enable: bool):
+    _check(lib().tfhe_stage_timing(1 if enable else 0))
+
+
+def tfhe_stage_times() -> dict:
+    """{stage: (total_ms, launches)} of the launches recorded since the last read."""
+    ms = (ctypes.c_double * 3)()
+    n = (ctypes.c_int64 * 3)()
+    _check(lib().tfhe_stage_times(ms, n))
+    return {STAGES[k]: (ms[k], n[k]) for k in range(3)}

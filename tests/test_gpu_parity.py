@@ -1,0 +1,287 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle.
+
+All arithmetic is mod 2^32 and exact, so every comparison is bit for bit.
+Inputs are seeded synthetic plaintexts (paper_1911_07101_amd.workloads); each
+side generates keys and ciphertexts itself from the same seeds (the library's
+key generation is checked byte-identical to the oracle's on the CPU).
+"""
+import os
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1911_07101_amd import tfhe, workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+M32 = 1 << 32
+MU = 1 << 29
+TRUTH = {"NAND": lambda a, b: 1 - (a & b), "AND": lambda a, b: a & b, "OR": lambda a, b: a | b,
+         "NOR": lambda a, b: 1 - (a | b), "XOR": lambda a, b: a ^ b, "XNOR": lambda a, b: 1 - (a ^ b),
+         "ANDNY": lambda a, b: (1 - a) & b, "ANDYN": lambda a, b: a & (1 - b),
+         "ORNY": lambda a, b: (1 - a) | b, "ORYN": lambda a, b: a | (1 - b)}
+
+
+def say(msg):
+    print(f"[gpu-parity] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+    if not _t.cuda.is_available():
+        pytest.skip("no GPU")
+    return _t
+
+
+def s32(x):
+    x = np.asarray(x, dtype=np.int64) % M32
+    return np.where(x >= M32 // 2, x - M32, x)
+
+
+def bits_of(phase):
+    return (s32(phase) > 0).astype(np.uint8)
+
+
+_KEYS = {}
+
+
+def keys_for(cfg_name, torch, params=None, seed=None):
+    """(library secret key, library eval key, oracle keys) for a config."""
+    params = params or wl.CONFIGS[cfg_name]["params"]
+    seed = seed if seed is not None else wl.CONFIGS[cfg_name]["key_seed"]
+    k = (cfg_name, tuple(sorted(params.items())), seed)
+    if k not in _KEYS:
+        say(f"keygen {cfg_name} n={params['n']} N={params['N']} seed={seed:#x}")
+        sk, ek = tfhe.tfhe_keygen_from_seed(params, seed, 0)
+        ok = oracle.Keys(params, seed)
+        _KEYS[k] = (sk, ek, ok)
+    return _KEYS[k]
+
+
+# ------------------------------------------------------------ transform
+
+PRODUCT_PARAMS = {
+    256: dict(n=4, N=256, l=3, bg_bit=7, ks_t=2, ks_basebit=2, alpha_lwe=0.0, alpha_bk=0.0),
+    512: dict(n=4, N=512, l=3, bg_bit=7, ks_t=2, ks_basebit=2, alpha_lwe=0.0, alpha_bk=0.0),
+    1024: dict(n=4, N=1024, l=3, bg_bit=7, ks_t=2, ks_basebit=2, alpha_lwe=0.0, alpha_bk=0.0),
+    2048: dict(n=4, N=2048, l=2, bg_bit=10, ks_t=2, ks_basebit=2, alpha_lwe=0.0, alpha_bk=0.0),
+}
+
+
+@pytest.mark.parametrize("N", [256, 512, 1024, 2048])
+def test_negacyclic_product_exact(torch, N):
+    """The fp64 NTT product equals the schoolbook product mod 2^32, including
+    inputs at the extremes of the exactness bound."""
+    p = PRODUCT_PARAMS[N]
+    _, ek, _ = keys_for(f"product{N}", torch, p, 7)
+    half = 1 << (p["bg_bit"] - 1)
+    rng = np.random.default_rng(N)
+    B = 7  # more than one block of polynomials and a ragged tail
+    d = rng.integers(-half, half, (B, N)).astype(np.int32)
+    b = rng.integers(0, M32, (B, N), dtype=np.uint64).astype(np.uint32)
+    # extremes: all digits -Bg/2 against coefficients whose 16-bit halves are
+    # both at their largest magnitude (hi = -2^15, lo = -2^15), and mixed signs
+    d[0] = -half
+    b[0] = np.uint32(0x7FFF8000)  # signed value 2^31 - 2^15: hi = 2^15, lo = -2^15
+    d[1] = -half
+    b[1] = np.uint32(0x80008000)  # -2^31 + 2^15 - 2^16... extreme negative halves
+    d[2] = np.where(np.arange(N) % 2 == 0, -half, half - 1)
+    b[2] = np.uint32(0x80000000)
+    say(f"negacyclic product N={N} B={B}")
+    out = tfhe.to_host(tfhe.tfhe_negacyclic_mul_batch(ek, torch.from_numpy(d).cuda(), tfhe.to_device(b)))
+    torch.cuda.synchronize()
+    for k in range(B):
+        ref = oracle.negacyclic_mul((d[k].astype(np.int64) % M32).astype(np.uint32), b[k])
+        assert np.array_equal(out[k], ref), f"polynomial {k}"
+
+
+# ------------------------------------------------------------ stages (toy)
+
+def test_blind_rotate_extract_parity_toy(torch):
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    rng = np.random.default_rng(11)
+    B = 37  # spans several blocks and a ragged tail
+    x = rng.integers(0, M32, (B, p["n"] + 1), dtype=np.uint64).astype(np.uint32)
+    x[0, :p["n"]] = 0  # a trivial sample (never rotated)
+    x[1, :] = 0
+    tv_gate = oracle.gate_testvec(p["N"])
+    say(f"blind rotate + extract toy B={B} (gate polynomial)")
+    got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x)))
+    ref = oracle.bootstrap_no_ks(ok, x, tv_gate)
+    assert np.array_equal(got, ref)
+    tv = rng.integers(0, M32, p["N"], dtype=np.uint64).astype(np.uint32)
+    say("blind rotate + extract toy with an arbitrary test polynomial")
+    got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x), tfhe.to_device(tv)))
+    assert np.array_equal(got, oracle.bootstrap_no_ks(ok, x, tv))
+
+
+def test_keyswitch_parity_toy(torch):
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    rng = np.random.default_rng(12)
+    for B in (1, 33, 70):
+        x = rng.integers(0, M32, (B, p["N"] + 1), dtype=np.uint64).astype(np.uint32)
+        say(f"keyswitch toy B={B}")
+        got = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, tfhe.to_device(x)))
+        assert np.array_equal(got, oracle.keyswitch(ok, x))
+
+
+@pytest.mark.parametrize("gate", list(TRUTH))
+def test_gate_bootstrap_toy(torch, gate):
+    cfg = wl.CONFIGS["toy"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    a, b = wl.gate_inputs(cfg["input_seed"], cfg["batch"])
+    ca = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), len(a))
+    oa = oracle.encrypt(p["n"], ok.s, cfg["input_seed"], p["alpha_lwe"], tfhe.encode_bits(a), 0)
+    assert np.array_equal(ca, oa)
+    say(f"gate {gate} toy B={len(a)}")
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, gate, tfhe.to_device(ca), tfhe.to_device(cb)))
+    ref = oracle.gate_bootstrap(ok, gate, ca, cb)
+    assert np.array_equal(got, ref)
+    assert np.array_equal(bits_of(oracle.phase(ok.s, got)), TRUTH[gate](a, b))
+
+
+def test_not_gate(torch):
+    rng = np.random.default_rng(3)
+    x = rng.integers(0, M32, (9, 65), dtype=np.uint64).astype(np.uint32)
+    got = tfhe.to_host(tfhe.tfhe_not_batch(tfhe.to_device(x)))
+    assert np.array_equal(got, oracle.not_gate(x))
+
+
+def test_determinism_and_batch_independence(torch):
+    cfg = wl.CONFIGS["toy"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    rng = np.random.default_rng(5)
+    B = 41
+    a, b = rng.integers(0, 2, B), rng.integers(0, 2, B)
+    ca = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 1, tfhe.encode_bits(a), 0))
+    cb = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 1, tfhe.encode_bits(b), B))
+    say("determinism toy")
+    r1 = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "XOR", ca, cb))
+    r2 = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "XOR", ca, cb))
+    assert np.array_equal(r1, r2)
+    parts = [tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "XOR", ca[s:e].contiguous(), cb[s:e].contiguous()))
+             for s, e in [(0, 1), (1, 6), (6, 41)]]
+    assert np.array_equal(np.concatenate(parts), r1)
+
+
+def test_relu_toy_all_values(torch):
+    """All 256 8-bit values through the ReLU unit on the toy parameters,
+    streamed in uneven gate windows."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    xs = np.arange(-128, 128)
+    bits = wl.to_bits(xs, 8)
+    ct = tfhe.tfhe_encrypt_torus(sk, 21, tfhe.encode_bits(bits.ravel())).reshape(256, 8, p["n"] + 1)
+    x = tfhe.to_device(ct)
+    y = torch.zeros_like(x)
+    total = 256 * 7
+    say("relu toy 256 values in 3 windows")
+    for s, e in [(0, 5), (5, 1000), (1000, total)]:
+        tfhe.glyph_relu_batch(ek, x, 8, y=y, gate_begin=s, gate_end=e)
+    got = tfhe.to_host(y)
+    ref = oracle.relu(ok, ct, 8)
+    assert np.array_equal(got, ref)
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(256, 8)
+    assert np.array_equal(wl.from_bits(dec), np.maximum(xs, 0))
+
+
+# ---------------------------------------------------- full-size workloads
+
+def test_tfhe128_nand_4096(torch):
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    a, b = wl.gate_inputs(cfg["input_seed"], cfg["batch"])
+    ca = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), len(a))
+    say(f"NAND n=630 N=1024 B={len(a)}")
+    t0 = time.time()
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", tfhe.to_device(ca), tfhe.to_device(cb)))
+    say(f"  gpu {time.time() - t0:.2f}s")
+    assert np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, got)), 1 - (a & b))
+    idx = wl.sample_indices(cfg["input_seed"], len(a), cfg["sample"])
+    t0 = time.time()
+    ref = oracle.gate_bootstrap(ok, "NAND", ca[idx], cb[idx])
+    say(f"  oracle sample of {len(idx)} in {time.time() - t0:.1f}s")
+    assert np.array_equal(got[idx], ref)
+
+
+def test_mlp_relu_7680(torch):
+    cfg = wl.CONFIGS["mlp_relu"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)  # same parameter set, shared keys
+    xs = wl.int8_values(cfg["input_seed"], cfg["values"])
+    bits = wl.to_bits(xs, 8)
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(bits.ravel()))
+    ct = ct.reshape(cfg["values"], 8, p["n"] + 1)
+    say(f"relu n=630 V={cfg['values']} gates={cfg['values'] * 7}")
+    t0 = time.time()
+    y = tfhe.to_host(tfhe.glyph_relu_batch(ek, tfhe.to_device(ct), 8))
+    say(f"  gpu {time.time() - t0:.2f}s")
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, y.reshape(-1, p["n"] + 1))).reshape(-1, 8)
+    assert np.array_equal(wl.from_bits(dec), np.maximum(xs.astype(np.int64), 0))
+    gates = wl.sample_indices(cfg["input_seed"], cfg["values"] * 7, cfg["sample"])
+    ref = oracle.relu_gates(ok, ct, 8, gates)
+    got = np.stack([y[g // 7, g % 7] for g in gates])
+    assert np.array_equal(got, ref)
+    assert np.all(y[:, 7, :p["n"]] == 0) and np.all(y[:, 7, p["n"]] == M32 - MU)
+
+
+def test_lut3_n2048_8192(torch):
+    cfg = wl.CONFIGS["lut3_n2048"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("lut3_n2048", torch)
+    m = wl.messages(cfg["input_seed"], cfg["batch"], cfg["msg_bits"])
+    lut = wl.lut(cfg["input_seed"], cfg["msg_bits"])
+    tv = tfhe.tfhe_lut_testvec(p["N"], cfg["msg_bits"], lut)
+    assert np.array_equal(tv, oracle.lut_testvec(p["N"], cfg["msg_bits"], lut))
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], (m << 28).astype(np.uint32))
+    say(f"lut bootstrap n=750 N=2048 B={len(m)}")
+    t0 = time.time()
+    got = tfhe.to_host(tfhe.tfhe_lut_bootstrap_batch(ek, tfhe.to_device(ct), tfhe.to_device(tv)))
+    say(f"  gpu {time.time() - t0:.2f}s")
+    ph = tfhe.tfhe_decrypt_phase(sk, got).astype(np.int64)
+    assert np.array_equal(((ph + (1 << 27)) >> 28) & 15, lut[m])
+    idx = wl.sample_indices(cfg["input_seed"], len(m), cfg["sample"])
+    t0 = time.time()
+    ref = oracle.lut_bootstrap(ok, ct[idx], tv)
+    say(f"  oracle sample of {len(idx)} in {time.time() - t0:.1f}s")
+    assert np.array_equal(got[idx], ref)
+
+
+def test_planted_oracle_error_is_detected(torch):
+    """The comparison can fail: a single flipped bit in the oracle's copy of
+    the bootstrapping key (planted on the CPU) breaks bit-exact agreement."""
+    cfg = wl.CONFIGS["toy"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    bad = oracle.Keys(p, cfg["key_seed"])
+    bad.bk[12345] ^= np.uint32(1 << 20)
+    a, b = wl.gate_inputs(cfg["input_seed"], cfg["batch"])
+    ca = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), len(a))
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", tfhe.to_device(ca), tfhe.to_device(cb)))
+    assert np.array_equal(got, oracle.gate_bootstrap(ok, "NAND", ca, cb))
+    assert not np.array_equal(got, oracle.gate_bootstrap(bad, "NAND", ca, cb))
+
+
+def test_workspace_too_small_is_rejected(torch):
+    sk, ek, ok = keys_for("toy", torch)
+    x = tfhe.to_device(np.zeros((8, 65), np.uint32))
+    ws = torch.empty(tfhe.tfhe_workspace_bytes(ek, 8) - 256, dtype=torch.uint8, device="cuda:0")
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.tfhe_gate_bootstrap_batch(ek, "AND", x, x, workspace=ws)
+    assert ei.value.rc == tfhe.TFHE_EINVAL
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.tfhe_gate_bootstrap_batch(ek, 17, x, x)
+    assert ei.value.rc == tfhe.TFHE_EINVAL

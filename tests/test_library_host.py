@@ -1,0 +1,103 @@
+"""CPU checks of the GPU library: it loads, exports every symbol its header
+declares, and its host-side (client) steps -- key generation, encryption,
+test-polynomial construction, argument validation -- agree with the oracle,
+which shares no code with it."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1911_07101_amd import tfhe, workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "glyph_tfhe.h")
+TOY = wl.CONFIGS["toy"]["params"]
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^[A-Za-z_][\w\s\*]*?\b((?:tfhe|glyph)_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(tfhe.LIB_PATH)
+    names = declared_functions()
+    assert len(names) >= 20
+    for name in names:
+        assert hasattr(lib, name), name
+    # and the binding covers all of them
+    assert set(names) <= set(tfhe._SIGNATURES)
+
+
+@pytest.mark.parametrize("cfg", ["toy", "tfhe128_nand"])
+def test_secret_keygen_matches_oracle(cfg):
+    p = wl.CONFIGS[cfg]["params"]
+    seed = wl.CONFIGS[cfg]["key_seed"]
+    sk = tfhe.tfhe_secret_keygen(p, seed)
+    mine = tfhe.tfhe_export_keys(sk)
+    ref = oracle.Keys(p, seed)
+    assert np.array_equal(mine["s"], ref.s)
+    assert np.array_equal(mine["S"], ref.S)
+    assert np.array_equal(mine["bk"], ref.bk)
+    assert np.array_equal(mine["ksk"], ref.ksk)
+
+
+def test_secret_keygen_matches_oracle_lut_params_small():
+    # the N = 2048, l = 2, Bg = 2^10 gadget and the 2^-45 noise floor, smaller n
+    p = dict(wl.CONFIGS["lut3_n2048"]["params"], n=24)
+    sk = tfhe.tfhe_secret_keygen(p, 99)
+    mine = tfhe.tfhe_export_keys(sk)
+    ref = oracle.Keys(p, 99)
+    for k in ("s", "S", "bk", "ksk"):
+        assert np.array_equal(mine[k], getattr(ref, k)), k
+
+
+def test_encryption_and_phase_match_oracle():
+    sk = tfhe.tfhe_secret_keygen(TOY, 5)
+    ref = oracle.Keys(TOY, 5)
+    mu = np.arange(300, dtype=np.uint32) * np.uint32(14318181)
+    ct = tfhe.tfhe_encrypt_torus(sk, 77, mu, first_index=1000)
+    assert np.array_equal(ct, oracle.encrypt(TOY["n"], ref.s, 77, TOY["alpha_lwe"], mu, 1000))
+    assert np.array_equal(tfhe.tfhe_decrypt_phase(sk, ct), oracle.phase(ref.s, ct))
+    ext = np.random.default_rng(1).integers(0, 2**32, (7, TOY["N"] + 1), dtype=np.uint64).astype(np.uint32)
+    assert np.array_equal(tfhe.tfhe_decrypt_phase(sk, ext, key_kind=1), oracle.phase(ref.S, ext))
+
+
+def test_lut_testvec_matches_oracle():
+    rng = np.random.default_rng(4)
+    for N, bits in [(256, 3), (2048, 3), (1024, 2), (512, 4)]:
+        lut = rng.integers(0, 1 << bits, 1 << bits).astype(np.uint32)
+        assert np.array_equal(tfhe.tfhe_lut_testvec(N, bits, lut), oracle.lut_testvec(N, bits, lut))
+    with pytest.raises(tfhe.TfheError):
+        tfhe.tfhe_lut_testvec(256, 3, np.array([8] * 8, np.uint32))
+
+
+@pytest.mark.parametrize("change,rc", [
+    (dict(N=768), tfhe.TFHE_EUNSUPPORTED),
+    (dict(N=4096), tfhe.TFHE_EUNSUPPORTED),
+    (dict(l=5, bg_bit=7), tfhe.TFHE_EUNSUPPORTED),         # l * bg_bit > 32
+    (dict(N=2048, l=3, bg_bit=10), tfhe.TFHE_EUNSUPPORTED),  # exactness bound
+    (dict(ks_t=17, ks_basebit=2), tfhe.TFHE_EUNSUPPORTED),
+    (dict(ks_basebit=9, ks_t=2), tfhe.TFHE_EUNSUPPORTED),
+    (dict(n=0), tfhe.TFHE_EUNSUPPORTED),
+    (dict(alpha_bk=-1.0), tfhe.TFHE_EINVAL),
+])
+def test_parameter_validation(change, rc):
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.tfhe_secret_keygen(dict(TOY, **change), 1)
+    assert ei.value.rc == rc
+
+
+def test_upload_without_gfx950_device_fails_cleanly():
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    sk = tfhe.tfhe_secret_keygen(TOY, 1)
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.tfhe_eval_key_upload(sk, 0)
+    assert ei.value.rc == tfhe.TFHE_EDEVICE
