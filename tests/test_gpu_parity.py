@@ -237,6 +237,43 @@ def test_mlp_relu_7680(torch):
     assert np.all(y[:, 7, :p["n"]] == 0) and np.all(y[:, 7, p["n"]] == M32 - MU)
 
 
+def test_conv_relu_streamed(torch):
+    """207,360 8-bit values (60 x 6 x 24 x 24), 1,451,520 ReLU gates streamed
+    through calls of 16,384 gates; every output decrypts to max(x, 0) and a
+    sample drawn across many calls matches the oracle bit for bit."""
+    cfg = wl.CONFIGS["conv_relu"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    V, step = cfg["values"], cfg["gates_per_call"]
+    total = V * 7
+    xs = wl.int8_values(cfg["input_seed"], V)
+    bits = wl.to_bits(xs, 8)
+    say(f"conv relu: encrypting {V * 8} bits")
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(bits.ravel()))
+    x = tfhe.to_device(ct.reshape(V, 8, p["n"] + 1))
+    y = torch.empty_like(x)
+    ws = tfhe.alloc_workspace(ek, step)
+    t0 = time.time()
+    calls = 0
+    for begin in range(0, total, step):
+        tfhe.glyph_relu_batch(ek, x, 8, y=y, gate_begin=begin, gate_end=min(begin + step, total), workspace=ws)
+        calls += 1
+        if calls % 16 == 0:
+            torch.cuda.synchronize()
+            say(f"  {calls} calls, {min(begin + step, total)} gates, {time.time() - t0:.1f}s")
+    torch.cuda.synchronize()
+    say(f"  gpu {calls} calls in {time.time() - t0:.1f}s")
+    yh = tfhe.to_host(y)
+    del x, y
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, yh.reshape(-1, p["n"] + 1))).reshape(V, 8)
+    assert np.array_equal(wl.from_bits(dec), np.maximum(xs.astype(np.int64), 0))
+    gates = wl.sample_indices(cfg["input_seed"], total, cfg["sample"])
+    assert len(np.unique(gates // step)) > 20  # the sample spans many calls
+    ref = oracle.relu_gates(ok, ct.reshape(V, 8, p["n"] + 1), 8, gates)
+    got = np.stack([yh[g // 7, g % 7] for g in gates])
+    assert np.array_equal(got, ref)
+
+
 def test_lut3_n2048_8192(torch):
     cfg = wl.CONFIGS["lut3_n2048"]
     p = cfg["params"]
