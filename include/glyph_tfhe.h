@@ -50,8 +50,9 @@ enum {
  * Supported: N in {256, 512, 1024, 2048}; 1 <= n <= 4096; 2 <= bg_bit,
  * l * bg_bit <= 32 and 2l * N * 2^(bg_bit-1) <= 2^22 (every coefficient of a
  * product of digits by a 16-bit half of the key then stays within 2^37, which
- * the NTT prime resolves exactly); ks_t * ks_basebit <= 32,
- * 1 <= ks_basebit <= 8. */
+ * the NTT prime resolves exactly); ks_t * ks_basebit <= 32 and
+ * ks_t * 2^ks_basebit <= 64 (the key rows of one coefficient fit the key-switch
+ * kernel's LDS stage). */
 typedef struct {
   int32_t n;          /* LWE dimension */
   int32_t N;          /* TRLWE ring degree */

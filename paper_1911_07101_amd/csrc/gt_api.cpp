@@ -36,9 +36,11 @@ int check_params(const tfhe_params& p) {
   const double bound = 2.0 * p.l * p.N * static_cast<double>(1u << (p.bg_bit - 1));
   if (bound > 4194304.0)
     return fail(TFHE_EUNSUPPORTED, "2l*N*Bg/2 = %.0f exceeds 2^22 (exactness bound of the transform)", bound);
-  if (p.ks_basebit < 1 || p.ks_basebit > 8 || p.ks_t < 1 || p.ks_t * p.ks_basebit > 32)
-    return fail(TFHE_EUNSUPPORTED, "key switching t=%d basebit=%d: need 1<=basebit<=8, t*basebit<=32",
-                p.ks_t, p.ks_basebit);
+  if (p.ks_basebit < 1 || p.ks_basebit > 6 || p.ks_t < 1 || p.ks_t * p.ks_basebit > 32 ||
+      p.ks_t * (1 << p.ks_basebit) > 64)
+    return fail(TFHE_EUNSUPPORTED,
+                "key switching t=%d basebit=%d: need t*basebit <= 32 and t*2^basebit <= 64", p.ks_t,
+                p.ks_basebit);
   if (!(p.alpha_lwe >= 0.0) || !(p.alpha_bk >= 0.0) || !(p.alpha_ks >= 0.0))
     return fail(TFHE_EINVAL, "noise parameters must be >= 0");
   return TFHE_OK;

@@ -334,27 +334,36 @@ __global__ __launch_bounds__(256, 2) void blind_rotate_kernel(
 }
 
 // ------------------------------------------------------- key switching
-// Block = 256 columns of the output x KS_CB samples.  Each thread keeps the
-// running output word of its column for every sample of the block; for each
-// input coefficient and digit the (uniform) digit of every sample selects a
-// key row, read coalesced across the columns and shared by the samples
-// through L1.
-constexpr int KS_CB = 32;
-constexpr int KS_ICH = 32;
+// One wave per block covers 64 output columns of KS_CB samples.  Each lane
+// keeps the running output word of its column for every sample.  For each
+// input coefficient i the block stages the key rows of all t digits and all
+// non-zero digit values, plus an all-zero row for digit value 0, in LDS
+// ([t][base][64] words); the (wave-uniform) digit of each sample then selects
+// its row with one LDS read and one subtraction.  The key rows are read from
+// global memory once per block and shared by the KS_CB samples.
+constexpr int KS_CB = 32;    // samples per block
+constexpr int KS_COLS = 64;  // output columns per block (one wave)
+constexpr int KS_ICH = 16;   // input coefficients staged per round
+constexpr int KS_MAXROWS = 64;  // t * 2^basebit rows of one coefficient, at most
 
-__global__ __launch_bounds__(256) void keyswitch_kernel(const uint32_t* __restrict__ in,
-                                                        const uint32_t* __restrict__ ksk,
-                                                        uint32_t* __restrict__ out, int n, int N,
-                                                        int ks_t, int basebit, int64_t B, int mode,
-                                                        int32_t bits, int64_t gate_begin) {
+template <int MAXROWS>
+__global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restrict__ in,
+                                                       const uint32_t* __restrict__ ksk,
+                                                       uint32_t* __restrict__ out, int n, int N,
+                                                       int ks_t, int basebit, int64_t B, int mode,
+                                                       int32_t bits, int64_t gate_begin) {
   __shared__ uint32_t s_in[KS_CB][KS_ICH];
+  __shared__ uint32_t s_rows[2][MAXROWS][KS_COLS];
+  const int lane = threadIdx.x;
   const int64_t c0 = static_cast<int64_t>(blockIdx.x) * KS_CB;
-  const int col = blockIdx.y * 256 + threadIdx.x;
+  const int col = blockIdx.y * KS_COLS + lane;
   const bool col_ok = col <= n;
   const int prec = ks_t * basebit;
   const uint32_t round = prec < 32 ? (1u << (31 - prec)) : 0u;
-  const int vals = (1 << basebit) - 1;
+  const int base = 1 << basebit;
+  const int vals = base - 1;
   const size_t row = static_cast<size_t>(n) + 1;
+  const int nrows = ks_t * base;  // rows staged per coefficient, value 0 included
 
   uint32_t acc[KS_CB];
 #pragma unroll
@@ -363,27 +372,49 @@ __global__ __launch_bounds__(256) void keyswitch_kernel(const uint32_t* __restri
     acc[k] = (col == n && c < B) ? in[c * (N + 1) + N] : 0u;
   }
 
+  // rows of coefficient i, (j, v) at j * base + v, fetched into registers
+  // one coefficient ahead and written to LDS after the current one is used
+  uint32_t pf[MAXROWS];
+  auto fetch = [&](int i) {
+    const uint32_t* krow_i = ksk + static_cast<size_t>(i) * ks_t * vals * row + col;
+#pragma unroll
+    for (int r = 0; r < MAXROWS; r++) {
+      const int j = r >> basebit, v = r & (base - 1);
+      pf[r] = (r < nrows && v != 0 && col_ok) ? krow_i[(static_cast<size_t>(j) * vals + (v - 1)) * row] : 0u;
+    }
+  };
+  auto put = [&](int b) {
+#pragma unroll
+    for (int r = 0; r < MAXROWS; r++)
+      if (r < nrows) s_rows[b][r][lane] = pf[r];
+  };
+
   for (int i0 = 0; i0 < N; i0 += KS_ICH) {
     __syncthreads();
-    for (int idx = threadIdx.x; idx < KS_CB * KS_ICH; idx += 256) {
+    for (int idx = lane; idx < KS_CB * KS_ICH; idx += KS_COLS) {
       const int k = idx / KS_ICH, ii = idx % KS_ICH;
       const int64_t c = c0 + k;
       s_in[k][ii] = (c < B && i0 + ii < N) ? in[c * (N + 1) + i0 + ii] : 0u;
     }
-    __syncthreads();
     const int iend = min(KS_ICH, N - i0);
+    fetch(i0);
+    put(0);
+    __syncthreads();
     for (int ii = 0; ii < iend; ii++) {
-      const int i = i0 + ii;
-      const uint32_t* krow_i = ksk + static_cast<size_t>(i) * ks_t * vals * row + col;
-#pragma unroll
+      const int b = ii & 1;
+      const bool more = ii + 1 < iend;
+      if (more) fetch(i0 + ii + 1);
+#pragma unroll 4
       for (int k = 0; k < KS_CB; k++) {
         const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
         const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
         for (int j = 0; j < ks_t; j++) {
           const uint32_t v = (r >> ((ks_t - 1 - j) * basebit)) & static_cast<uint32_t>(vals);
-          if (v != 0 && col_ok) acc[k] -= krow_i[(static_cast<size_t>(j) * vals + (v - 1)) * row];
+          acc[k] -= s_rows[b][j * base + v][lane];
         }
       }
+      if (more) put(b ^ 1);
+      __syncthreads();
     }
   }
 
@@ -534,9 +565,16 @@ int launch_blind_rotate(const tfhe_eval_key* ek, const Workspace& ws, const uint
 int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B, int mode,
                      int32_t bits, int64_t gate_begin, void* stream) {
   const tfhe_params& p = ek->p;
-  dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + 255) / 256));
-  hipLaunchKernelGGL(keyswitch_kernel, grid, dim3(256), 0, static_cast<hipStream_t>(stream), in, ek->ksk,
-                     out, p.n, p.N, p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
+  if (p.ks_t * (1 << p.ks_basebit) > KS_MAXROWS)
+    return fail(TFHE_EUNSUPPORTED, "key switching with t * 2^basebit = %d > %d rows per coefficient",
+                p.ks_t * (1 << p.ks_basebit), KS_MAXROWS);
+  dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
+  if (p.ks_t * (1 << p.ks_basebit) <= 32)
+    hipLaunchKernelGGL(keyswitch_kernel<32>, grid, dim3(KS_COLS), 0, static_cast<hipStream_t>(stream), in,
+                       ek->ksk, out, p.n, p.N, p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
+  else
+    hipLaunchKernelGGL(keyswitch_kernel<64>, grid, dim3(KS_COLS), 0, static_cast<hipStream_t>(stream), in,
+                       ek->ksk, out, p.n, p.N, p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   return launch_status("keyswitch_kernel");
 }
 

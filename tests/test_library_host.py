@@ -84,6 +84,7 @@ def test_lut_testvec_matches_oracle():
     (dict(N=2048, l=3, bg_bit=10), tfhe.TFHE_EUNSUPPORTED),  # exactness bound
     (dict(ks_t=17, ks_basebit=2), tfhe.TFHE_EUNSUPPORTED),
     (dict(ks_basebit=9, ks_t=2), tfhe.TFHE_EUNSUPPORTED),
+    (dict(ks_t=16, ks_basebit=3), tfhe.TFHE_EUNSUPPORTED),    # 128 key rows per coefficient
     (dict(n=0), tfhe.TFHE_EUNSUPPORTED),
     (dict(alpha_bk=-1.0), tfhe.TFHE_EINVAL),
 ])
