@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "gt_internal.h"
+#include "gt_layout.hpp"
 
 namespace gt {
 
@@ -246,7 +247,7 @@ void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
   const BkCtx& c = *static_cast<BkCtx*>(vctx);
   const int N = c.p->N;
   const int logn = ilog2(N);
-  const int loge = logn >= 10 ? 4 : logn - 6;
+  const int loge = log_values_per_thread(logn);
   const int E = 1 << loge, T = N >> loge;
   const uint64_t ninv = powmod_u64(static_cast<uint64_t>(N), kPrimeU - 2);
   std::vector<uint64_t> hi(N), lo(N);
@@ -266,11 +267,13 @@ void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
     const int64_t ir = row / 2, q = row % 2;
     double* dst_hi = c.out + (ir * 4 + 2 * q) * N;
     double* dst_lo = dst_hi + N;
+    // thread t's values e = 2h, 2h+1 are adjacent: layout [E/2][T][2]
     for (int t = 0; t < T; t++)
       for (int e = 0; e < E; e++) {
         const int j = e | (t << loge);  // transform-domain index held by (t, e)
-        dst_hi[e * T + t] = static_cast<double>(mulmod_u64(hi[j], ninv));
-        dst_lo[e * T + t] = static_cast<double>(mulmod_u64(lo[j], ninv));
+        const int slot = (e >> 1) * 2 * T + 2 * t + (e & 1);
+        dst_hi[slot] = static_cast<double>(mulmod_u64(hi[j], ninv));
+        dst_lo[slot] = static_cast<double>(mulmod_u64(lo[j], ninv));
       }
   }
 }

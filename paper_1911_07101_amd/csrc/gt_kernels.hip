@@ -32,6 +32,12 @@ namespace {
 
 constexpr uint32_t kMu = 0x20000000u;  // 1/8
 
+// minimum waves per SIMD the blind-rotation kernel is compiled for (sets its
+// register budget: 2 -> 256 VGPRs, 3 -> 168)
+#ifndef GT_BR_WAVES_PER_SIMD
+#define GT_BR_WAVES_PER_SIMD 2
+#endif
+
 template <int B, int E, class F>
 __device__ __forceinline__ void static_for(F&& f) {
   if constexpr (B < E) {
@@ -73,30 +79,65 @@ __device__ __forceinline__ void transpose(double (&x)[Lay::E], int t, double* sc
   poly_sync<Lay::T>();
 }
 
+// Offset of stage k's twiddles within a pass's batch: the stages before it
+// (descending bits for the forward transform, ascending for the inverse) use
+// E >> (b + 1) twiddles each, b the stage's bit within the pass window.
+template <class Lay>
+constexpr int tw_offset(int p, int k, bool fwd) {
+  int off = 0;
+  for (int q = 0; q < k; q++) {
+    const int s = fwd ? Lay::hi(p) - 1 - q : Lay::lo(p) + q;
+    off += Lay::E >> (s - Lay::win(p) + 1);
+  }
+  return off;
+}
+
 // Forward negacyclic NTT (Cooley-Tukey butterflies, twiddle psi^brv(k) for the
 // block of coefficient j at stage s: k = N/2^(s+1) + j/2^(s+1)).  In: pass-0
 // (coefficient) layout; out: last-pass (transform) layout.  |in| < 2^10 gives
-// |out| < 2^43 (each stage adds at most 0.75P + 2^35).
-template <class Lay>
+// |out| < 2^43 (each stage adds at most 0.75P + 2^35).  The twiddles of a pass
+// are fetched together before its butterflies: pass 0's are the same for every
+// thread (tw_uniform, read through the scalar cache), the others come from
+// the LDS copy tw.  SMALL_IN: inputs are below 2^10 in magnitude, so the first
+// stage's products are exact without the low part.
+template <class Lay, bool SMALL_IN>
 __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* scr,
-                                            const double* __restrict__ tw) {
-  constexpr int N = Lay::N, LOGE = Lay::LOGE;
+                                            const double* __restrict__ tw,
+                                            const double* __restrict__ tw_uniform) {
+  constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = decltype(PI)::value;
     constexpr int w = Lay::win(p);
+    constexpr int NS = Lay::hi(p) - Lay::lo(p);
     if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w>(x, t, scr);
-    static_for<0, Lay::hi(p) - Lay::lo(p)>([&](auto SI) {
+    // twiddles of all stages of the pass: stage si uses z[off(si) .. off(si) + G(si))
+    double z[E];
+    static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
       constexpr int b = s - w;
-      const int base = (N >> (s + 1)) + ((t >> w) << (LOGE - b - 1));
-      static_for<0, (Lay::E >> (b + 1))>([&](auto GI) {
+      constexpr int G = E >> (b + 1);
+      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, true);
+      static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
-        const double z = tw[base + g];
+        if constexpr (p == 0)
+          z[off + g] = tw_uniform[(N >> (s + 1)) + g];
+        else
+          z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
+      });
+    });
+    static_for<0, NS>([&](auto SI) {
+      constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
+      constexpr int b = s - w;
+      constexpr int G = E >> (b + 1);
+      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, true);
+      constexpr bool small = SMALL_IN && p == 0 && decltype(SI)::value == 0;
+      static_for<0, G>([&](auto GI) {
+        constexpr int g = decltype(GI)::value;
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
           const double u = x[e];
-          const double v = mulmod(x[e2], z);
+          const double v = small ? mulmod_small(x[e2], z[off + g]) : mulmod(x[e2], z[off + g]);
           x[e] = u + v;
           x[e2] = u - v;
         });
@@ -110,39 +151,57 @@ __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* 
 // coefficient layout, |out| < 2^(38 + LOGN) (sums double per stage).
 template <class Lay>
 __device__ __forceinline__ void ntt_inverse(double (&x)[Lay::E], int t, double* scr,
-                                            const double* __restrict__ tw) {
-  constexpr int N = Lay::N, LOGE = Lay::LOGE;
+                                            const double* __restrict__ tw,
+                                            const double* __restrict__ tw_uniform) {
+  constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = Lay::NPASS - 1 - decltype(PI)::value;
     constexpr int w = Lay::win(p);
+    constexpr int NS = Lay::hi(p) - Lay::lo(p);
     if constexpr (p < Lay::NPASS - 1) transpose<Lay, Lay::win(p + 1), w>(x, t, scr);
-    static_for<0, Lay::hi(p) - Lay::lo(p)>([&](auto SI) {
+    // stage si (ascending bit s = lo + si) uses z[off(si) .. off(si) + G(si))
+    double z[E];
+    static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::lo(p) + decltype(SI)::value;
       constexpr int b = s - w;
-      const int base = (N >> (s + 1)) + ((t >> w) << (LOGE - b - 1));
-      static_for<0, (Lay::E >> (b + 1))>([&](auto GI) {
+      constexpr int G = E >> (b + 1);
+      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, false);
+      static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
-        const double z = tw[base + g];
+        if constexpr (p == 0)
+          z[off + g] = tw_uniform[(N >> (s + 1)) + g];
+        else
+          z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
+      });
+    });
+    static_for<0, NS>([&](auto SI) {
+      constexpr int s = Lay::lo(p) + decltype(SI)::value;
+      constexpr int b = s - w;
+      constexpr int G = E >> (b + 1);
+      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, false);
+      static_for<0, G>([&](auto GI) {
+        constexpr int g = decltype(GI)::value;
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
           const double u = x[e];
           const double v = x[e2];
           x[e] = u + v;
-          x[e2] = mulmod(u - v, z);
+          x[e2] = mulmod(u - v, z[off + g]);
         });
       });
     });
   });
 }
 
-// coefficient j of X^e * p for e in [0, 2N), p in LDS
+// coefficient j of X^e * p for e in [0, 2N), p in LDS: p[(j - e) mod N],
+// negated when the index wrapped or when e >= N (X^N = -1), without branches
 template <int N>
 __device__ __forceinline__ uint32_t rot_coef(const uint32_t* p, uint32_t e, int j) {
-  const int sh = static_cast<int>(e & (N - 1));
-  const int src = j - sh;
-  uint32_t v = src >= 0 ? p[src] : 0u - p[src + N];
-  return (e & N) ? 0u - v : v;
+  const int src = j - static_cast<int>(e & (N - 1));
+  const uint32_t v = p[src & (N - 1)];
+  const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e / N) & 1u));
+  return (v ^ m) - m;
 }
 
 // ------------------------------------------------------------ prep kernel
@@ -212,7 +271,7 @@ struct BrCfg {
 };
 
 template <int LOGN>
-__global__ __launch_bounds__(256, 2) void blind_rotate_kernel(
+__global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
     const double* __restrict__ bk, const double* __restrict__ tw_fwd_g,
     const double* __restrict__ tw_inv_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
@@ -256,8 +315,8 @@ __global__ __launch_bounds__(256, 2) void blind_rotate_kernel(
       uint32_t v;
       if (testvec == nullptr) {
         const int src = j - static_cast<int>(e0 & (N - 1));
-        v = src >= 0 ? kMu : 0u - kMu;
-        if (e0 & N) v = 0u - v;
+        const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e0 / N) & 1u));
+        v = (kMu ^ m) - m;
       } else {
         v = rot_coef<N>(testvec, e0, j);
       }
@@ -296,12 +355,31 @@ __global__ __launch_bounds__(256, 2) void blind_rotate_kernel(
 #pragma unroll
         for (int e = 0; e < E; e++)
           x[e] = static_cast<double>(static_cast<int32_t>((D[e] >> shift) & dmask) - static_cast<int32_t>(half));
-        ntt_forward<Lay>(x, t, scr, twf);
-        const double* bkr = bki + static_cast<size_t>(q * l + jj) * 4 * N + t;
+        // key row r = q*l + jj: four output polynomials, each stored as
+        // [E/2][T][2] so a thread's pair of values is one 16-byte load
+        const double2* bkr =
+            reinterpret_cast<const double2*>(bki + static_cast<size_t>(q * l + jj) * 4 * N) + t;
+        ntt_forward<Lay, true>(x, t, scr, twf, tw_fwd_g);
+        double2 w[E / 2];
 #pragma unroll
-        for (int o = 0; o < 4; o++)
+        for (int h = 0; h < E / 2; h++) w[h] = bkr[h * T];
 #pragma unroll
-          for (int e = 0; e < E; e++) acc[o][e] += mulmod(x[e], bkr[o * N + e * T]);
+        for (int o = 0; o < 4; o++) {
+          double2 wn[E / 2];
+          if (o < 3) {
+#pragma unroll
+            for (int h = 0; h < E / 2; h++) wn[h] = bkr[(o + 1) * (N / 2) + h * T];
+          }
+#pragma unroll
+          for (int h = 0; h < E / 2; h++) {
+            acc[o][2 * h] += mulmod(x[2 * h], w[h].x);
+            acc[o][2 * h + 1] += mulmod(x[2 * h + 1], w[h].y);
+          }
+          if (o < 3) {
+#pragma unroll
+            for (int h = 0; h < E / 2; h++) w[h] = wn[h];
+          }
+        }
       }
     }
 
@@ -309,7 +387,7 @@ __global__ __launch_bounds__(256, 2) void blind_rotate_kernel(
     for (int o = 0; o < 4; o++) {
 #pragma unroll
       for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
-      ntt_inverse<Lay>(acc[o], t, scr, twi);
+      ntt_inverse<Lay>(acc[o], t, scr, twi, tw_inv_g);
 #pragma unroll
       for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
     }
@@ -346,14 +424,18 @@ constexpr int KS_COLS = 64;  // output columns per block (one wave)
 constexpr int KS_ICH = 16;   // input coefficients staged per round
 constexpr int KS_MAXROWS = 64;  // t * 2^basebit rows of one coefficient, at most
 
-template <int MAXROWS>
+// KT > 0: digit count and base fixed at compile time (the digit loop unrolls);
+// KT = 0: runtime ks_t / basebit.  MAXROWS >= ks_t * 2^basebit.
+template <int MAXROWS, int KT, int KBB>
 __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restrict__ in,
                                                        const uint32_t* __restrict__ ksk,
                                                        uint32_t* __restrict__ out, int n, int N,
-                                                       int ks_t, int basebit, int64_t B, int mode,
+                                                       int ks_t_rt, int basebit_rt, int64_t B, int mode,
                                                        int32_t bits, int64_t gate_begin) {
   __shared__ uint32_t s_in[KS_CB][KS_ICH];
   __shared__ uint32_t s_rows[2][MAXROWS][KS_COLS];
+  const int ks_t = KT > 0 ? KT : ks_t_rt;
+  const int basebit = KT > 0 ? KBB : basebit_rt;
   const int lane = threadIdx.x;
   const int64_t c0 = static_cast<int64_t>(blockIdx.x) * KS_CB;
   const int col = blockIdx.y * KS_COLS + lane;
@@ -404,13 +486,29 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
       const int b = ii & 1;
       const bool more = ii + 1 < iend;
       if (more) fetch(i0 + ii + 1);
+      const uint32_t* rows = &s_rows[b][0][lane];
+      if constexpr (KT > 0) {
+#pragma unroll 8
+        for (int k = 0; k < KS_CB; k++) {
+          const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
+          const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
+          uint32_t sum = 0u;
+#pragma unroll
+          for (int j = 0; j < KT; j++) {
+            const uint32_t v = (r >> ((KT - 1 - j) * KBB)) & ((1u << KBB) - 1u);
+            sum += rows[((j << KBB) + v) * KS_COLS];
+          }
+          acc[k] -= sum;
+        }
+      } else {
 #pragma unroll 4
-      for (int k = 0; k < KS_CB; k++) {
-        const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
-        const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
-        for (int j = 0; j < ks_t; j++) {
-          const uint32_t v = (r >> ((ks_t - 1 - j) * basebit)) & static_cast<uint32_t>(vals);
-          acc[k] -= s_rows[b][j * base + v][lane];
+        for (int k = 0; k < KS_CB; k++) {
+          const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
+          const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
+          for (int j = 0; j < ks_t; j++) {
+            const uint32_t v = (r >> ((ks_t - 1 - j) * basebit)) & static_cast<uint32_t>(vals);
+            acc[k] -= rows[(j * base + v) * KS_COLS];
+          }
         }
       }
       if (more) put(b ^ 1);
@@ -475,9 +573,9 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double* __res
     xh[e] = static_cast<double>(hi);
     xl[e] = static_cast<double>(lo);
   }
-  ntt_forward<Lay>(xd, t, scr, twf);
-  ntt_forward<Lay>(xh, t, scr, twf);
-  ntt_forward<Lay>(xl, t, scr, twf);
+  ntt_forward<Lay, true>(xd, t, scr, twf, twf);
+  ntt_forward<Lay, false>(xh, t, scr, twf, twf);
+  ntt_forward<Lay, false>(xl, t, scr, twf, twf);
   // N^-1 mod P, folded into the products
   double ninv = 1.0;
   {
@@ -489,8 +587,8 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double* __res
     xh[e] = reduce(mulmod(de, xh[e]));
     xl[e] = reduce(mulmod(de, xl[e]));
   }
-  ntt_inverse<Lay>(xh, t, scr, twi);
-  ntt_inverse<Lay>(xl, t, scr, twi);
+  ntt_inverse<Lay>(xh, t, scr, twi, twi);
+  ntt_inverse<Lay>(xl, t, scr, twi, twi);
   if (!active) return;
   for (int e = 0; e < E; e++) {
     const int j = t + T * e;
@@ -569,12 +667,16 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
     return fail(TFHE_EUNSUPPORTED, "key switching with t * 2^basebit = %d > %d rows per coefficient",
                 p.ks_t * (1 << p.ks_basebit), KS_MAXROWS);
   dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
-  if (p.ks_t * (1 << p.ks_basebit) <= 32)
-    hipLaunchKernelGGL(keyswitch_kernel<32>, grid, dim3(KS_COLS), 0, static_cast<hipStream_t>(stream), in,
-                       ek->ksk, out, p.n, p.N, p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (p.ks_t == 8 && p.ks_basebit == 2)
+    hipLaunchKernelGGL((keyswitch_kernel<32, 8, 2>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
+                       p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
+  else if (p.ks_t * (1 << p.ks_basebit) <= 32)
+    hipLaunchKernelGGL((keyswitch_kernel<32, 0, 0>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
+                       p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   else
-    hipLaunchKernelGGL(keyswitch_kernel<64>, grid, dim3(KS_COLS), 0, static_cast<hipStream_t>(stream), in,
-                       ek->ksk, out, p.n, p.N, p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
+    hipLaunchKernelGGL((keyswitch_kernel<64, 0, 0>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
+                       p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   return launch_status("keyswitch_kernel");
 }
 

@@ -25,12 +25,16 @@
 
 namespace gt {
 
+// log2 of the values per thread for a ring of degree 2^logn (host and device)
+constexpr GL_HD int log_values_per_thread(int logn) { return logn >= 9 ? 3 : logn - 6; }
+
 template <int LOGN_>
 struct Layout {
   static constexpr int LOGN = LOGN_;
   static constexpr int N = 1 << LOGN;
-  // 16 values per thread from N = 1024 up, one wave of 64 threads below
-  static constexpr int LOGE = LOGN >= 10 ? 4 : LOGN - 6;
+  // 8 values per thread (4 at N = 256): the four transform-domain
+  // accumulators of an external product then take 64 registers per thread
+  static constexpr int LOGE = log_values_per_thread(LOGN);
   static constexpr int E = 1 << LOGE;
   static constexpr int LOGT = LOGN - LOGE;
   static constexpr int T = 1 << LOGT;

@@ -132,6 +132,19 @@ def test_keyswitch_parity_toy(torch):
         assert np.array_equal(got, oracle.keyswitch(ok, x))
 
 
+@pytest.mark.parametrize("ks_t,ks_basebit", [(4, 3), (16, 2), (2, 5)])
+def test_keyswitch_parity_other_digit_sizes(torch, ks_t, ks_basebit):
+    """The key switch for digit shapes other than t = 8, base 4 (the kernel's
+    runtime-shaped variants, 32 and 64 key rows per coefficient)."""
+    p = dict(wl.CONFIGS["toy"]["params"], n=40, ks_t=ks_t, ks_basebit=ks_basebit)
+    sk, ek, ok = keys_for(f"ks{ks_t}x{ks_basebit}", torch, p, 3)
+    rng = np.random.default_rng(ks_t * 10 + ks_basebit)
+    x = rng.integers(0, M32, (45, p["N"] + 1), dtype=np.uint64).astype(np.uint32)
+    say(f"keyswitch t={ks_t} basebit={ks_basebit}")
+    got = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, tfhe.to_device(x)))
+    assert np.array_equal(got, oracle.keyswitch(ok, x))
+
+
 @pytest.mark.parametrize("gate", list(TRUTH))
 def test_gate_bootstrap_toy(torch, gate):
     cfg = wl.CONFIGS["toy"]
