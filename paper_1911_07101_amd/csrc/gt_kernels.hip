@@ -61,9 +61,33 @@ __device__ __forceinline__ void poly_sync() {
   }
 }
 
-// bank swizzle of the transpose scratch (conflict-free for every pass layout
-// at N >= 1024 with 64-bit elements)
-__device__ __forceinline__ int swz(int j) { return j ^ ((j >> 4) & 15); }
+// bank swizzle of the transpose scratch: with 8 values per thread every pass
+// layout at N = 512..2048 reads and writes 64-bit elements without bank
+// conflicts (checked for 32 and 64 banks of 4 bytes); it permutes only the low
+// 5 bits, so it stays inside the polynomial
+__device__ __forceinline__ int swz(int j) { return j ^ (((j >> 3) ^ (j >> 7)) & 31); }
+
+// Position of twiddle k in the LDS copy of a twiddle table.  Stage s owns
+// k in [N/2^(s+1), N/2^s); in a pass other than the first, thread t reads the
+// stage's entries m = (t >> w) * G + g, g < G, so they are stored [g][t >> w]
+// to make the threads of a wave read consecutive words.  First-pass twiddles
+// are read uniformly from global memory and keep their natural place.
+template <class Lay>
+__host__ __device__ constexpr int tw_lds_slot(int k) {
+  if (k == 0) return 0;
+  int lg = 0;
+  while ((2 << lg) <= k) lg++;           // floor(log2 k)
+  const int s = Lay::LOGN - 1 - lg;      // stage of k
+  int p = 0;
+  while (!(Lay::lo(p) <= s && s < Lay::hi(p))) p++;
+  if (p == 0) return k;
+  const int b = s - Lay::win(p);
+  const int G = Lay::E >> (b + 1);
+  const int start = Lay::N >> (s + 1);
+  const int m = k - start;
+  const int rows = start / G;
+  return start + (m % G) * rows + m / G;
+}
 
 template <class Lay, int WFROM, int WTO>
 __device__ __forceinline__ void transpose(double (&x)[Lay::E], int t, double* scr) {
@@ -98,9 +122,10 @@ constexpr int tw_offset(int p, int k, bool fwd) {
 // |out| < 2^43 (each stage adds at most 0.75P + 2^35).  The twiddles of a pass
 // are fetched together before its butterflies: pass 0's are the same for every
 // thread (tw_uniform, read through the scalar cache), the others come from
-// the LDS copy tw.  SMALL_IN: inputs are below 2^10 in magnitude, so the first
+// tw: an LDS copy laid out by tw_lds_slot (TW_PERMUTED) or a natural-order
+// table in global memory.  SMALL_IN: inputs are below 2^10 in magnitude, so the first
 // stage's products are exact without the low part.
-template <class Lay, bool SMALL_IN>
+template <class Lay, bool SMALL_IN, bool TW_PERMUTED>
 __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* scr,
                                             const double* __restrict__ tw,
                                             const double* __restrict__ tw_uniform) {
@@ -121,6 +146,8 @@ __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* 
         constexpr int g = decltype(GI)::value;
         if constexpr (p == 0)
           z[off + g] = tw_uniform[(N >> (s + 1)) + g];
+        else if constexpr (TW_PERMUTED)
+          z[off + g] = tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
         else
           z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
       });
@@ -149,7 +176,7 @@ __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* 
 // Inverse transform without the 1/N factor (Gentleman-Sande butterflies,
 // twiddle psi^-brv(k)).  In: transform layout, |in| <= P/2 + 1; out:
 // coefficient layout, |out| < 2^(38 + LOGN) (sums double per stage).
-template <class Lay>
+template <class Lay, bool TW_PERMUTED>
 __device__ __forceinline__ void ntt_inverse(double (&x)[Lay::E], int t, double* scr,
                                             const double* __restrict__ tw,
                                             const double* __restrict__ tw_uniform) {
@@ -170,6 +197,8 @@ __device__ __forceinline__ void ntt_inverse(double (&x)[Lay::E], int t, double* 
         constexpr int g = decltype(GI)::value;
         if constexpr (p == 0)
           z[off + g] = tw_uniform[(N >> (s + 1)) + g];
+        else if constexpr (TW_PERMUTED)
+          z[off + g] = tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
         else
           z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
       });
@@ -267,7 +296,7 @@ struct BrCfg {
   using Lay = Layout<LOGN>;
   static constexpr int N = Lay::N, E = Lay::E, T = Lay::T;
   static constexpr int CPB = 256 / T;                // ciphertexts per block
-  static constexpr bool kTwLds = N <= 1024;          // twiddle tables in LDS
+  static constexpr bool kTwLds = true;               // twiddle tables in LDS
 };
 
 template <int LOGN>
@@ -292,7 +321,11 @@ __global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel
   const double* twf;
   const double* twi;
   if constexpr (C::kTwLds) {
-    for (int k = threadIdx.x; k < 2 * N; k += 256) s_tw[k] = k < N ? tw_fwd_g[k] : tw_inv_g[k - N];
+    for (int k = threadIdx.x; k < N; k += 256) {
+      const int slot = tw_lds_slot<Lay>(k);
+      s_tw[slot] = tw_fwd_g[k];
+      s_tw[N + slot] = tw_inv_g[k];
+    }
     __syncthreads();
     twf = s_tw;
     twi = s_tw + N;
@@ -359,7 +392,7 @@ __global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel
         // [E/2][T][2] so a thread's pair of values is one 16-byte load
         const double2* bkr =
             reinterpret_cast<const double2*>(bki + static_cast<size_t>(q * l + jj) * 4 * N) + t;
-        ntt_forward<Lay, true>(x, t, scr, twf, tw_fwd_g);
+        ntt_forward<Lay, true, C::kTwLds>(x, t, scr, twf, tw_fwd_g);
         double2 w[E / 2];
 #pragma unroll
         for (int h = 0; h < E / 2; h++) w[h] = bkr[h * T];
@@ -387,7 +420,7 @@ __global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel
     for (int o = 0; o < 4; o++) {
 #pragma unroll
       for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
-      ntt_inverse<Lay>(acc[o], t, scr, twi, tw_inv_g);
+      ntt_inverse<Lay, C::kTwLds>(acc[o], t, scr, twi, tw_inv_g);
 #pragma unroll
       for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
     }
@@ -531,6 +564,108 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
   }
 }
 
+// Key switching for t = 8 digits of 2 bits (16-bit precision).  A block of 4
+// waves covers 64 output columns of 4 x 32 samples.  For each input
+// coefficient i the block builds, in LDS, the pair tables
+//   PT[p][u][col] = KSK[i][2p][u >> 2] + KSK[i][2p+1][u & 3]   (row of value 0 = 0)
+// for the 4 digit pairs p and the 16 pair values u; a sample then needs 4
+// table reads for the 8 digits.  Tables are double-buffered across i; the key
+// rows are fetched one coefficient ahead.  Every table read, add and the
+// final subtraction are exact mod 2^32.
+constexpr int KS8_WAVES = 4;
+#ifndef GT_KS8_CB
+#define GT_KS8_CB 16
+#endif
+constexpr int KS8_CB = GT_KS8_CB;  // samples per wave
+
+__global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __restrict__ in,
+                                                             const uint32_t* __restrict__ ksk,
+                                                             uint32_t* __restrict__ out, int n, int N,
+                                                             int64_t B, int mode, int32_t bits,
+                                                             int64_t gate_begin) {
+  constexpr int ROWS = 24;              // 8 digits x 3 non-zero values
+  constexpr int TAB = 64;               // 4 pairs x 16 pair values
+  __shared__ uint32_t s_tab[2][TAB][KS_COLS];
+  __shared__ uint32_t s_in[KS8_WAVES * KS8_CB][KS_ICH];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = blockIdx.y * KS_COLS + lane;
+  const bool col_ok = col <= n;
+  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * (KS8_WAVES * KS8_CB);
+  const int64_t cw = c0 + wave * KS8_CB;
+  const size_t row = static_cast<size_t>(n) + 1;
+
+  uint32_t acc[KS8_CB];
+#pragma unroll
+  for (int k = 0; k < KS8_CB; k++) {
+    const int64_t c = cw + k;
+    acc[k] = (col == n && c < B) ? in[c * (N + 1) + N] : 0u;
+  }
+
+  // thread (wave, lane) fetches key rows wave*6 .. wave*6+5 of its column and
+  // builds table entries (pair = wave, all 16 values) -- the two digit rows a
+  // pair needs are rows 6*wave .. 6*wave+5, exactly this thread's fetch
+  uint32_t kr[6];
+  auto fetch = [&](int i) {
+    const uint32_t* base = ksk + static_cast<size_t>(i) * ROWS * row + col;
+#pragma unroll
+    for (int q = 0; q < 6; q++) kr[q] = col_ok ? base[static_cast<size_t>(wave * 6 + q) * row] : 0u;
+  };
+  auto build = [&](int b) {
+    // kr[0..2]: digit 2*wave, values 1..3; kr[3..5]: digit 2*wave+1, values 1..3
+#pragma unroll
+    for (int u = 0; u < 16; u++) {
+      const int v1 = u >> 2, v2 = u & 3;
+      const uint32_t a = v1 ? kr[v1 - 1] : 0u;
+      const uint32_t c = v2 ? kr[2 + v2] : 0u;
+      s_tab[b][wave * 16 + u][lane] = a + c;
+    }
+  };
+
+  fetch(0);
+  for (int i0 = 0; i0 < N; i0 += KS_ICH) {
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < KS8_WAVES * KS8_CB * KS_ICH; idx += 256) {
+      const int k = idx / KS_ICH, ii = idx % KS_ICH;
+      const int64_t c = c0 + k;
+      s_in[k][ii] = (c < B && i0 + ii < N) ? in[c * (N + 1) + i0 + ii] : 0u;
+    }
+    const int iend = min(KS_ICH, N - i0);
+    for (int ii = 0; ii < iend; ii++) {
+      const int i = i0 + ii;
+      const int b = i & 1;
+      build(b);
+      if (i + 1 < N) fetch(i + 1);
+      __syncthreads();
+      const uint32_t* tab = &s_tab[b][0][lane];
+#pragma unroll 8
+      for (int k = 0; k < KS8_CB; k++) {
+        const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[wave * KS8_CB + k][ii]);
+        const uint32_t r = (x + 0x8000u) >> 16;  // round to 16 bits, ties up
+        const uint32_t s0 = tab[(0 * 16 + ((r >> 12) & 15)) * KS_COLS];
+        const uint32_t s1 = tab[(1 * 16 + ((r >> 8) & 15)) * KS_COLS];
+        const uint32_t s2 = tab[(2 * 16 + ((r >> 4) & 15)) * KS_COLS];
+        const uint32_t s3 = tab[(3 * 16 + (r & 15)) * KS_COLS];
+        acc[k] -= (s0 + s1) + (s2 + s3);
+      }
+    }
+  }
+
+  if (!col_ok) return;
+#pragma unroll
+  for (int k = 0; k < KS8_CB; k++) {
+    const int64_t c = cw + k;
+    if (c >= B) break;
+    int64_t dst = c;
+    if (mode == kModeRelu) {
+      const int64_t g = gate_begin + c;
+      const int64_t v = g / (bits - 1), bit = g - v * (bits - 1);
+      dst = v * bits + bit;
+    }
+    out[dst * row + col] = acc[k];
+  }
+}
+
 __global__ __launch_bounds__(256) void relu_sign_kernel(uint32_t* __restrict__ y, int n, int32_t bits,
                                                         int64_t v_begin, int64_t count) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -573,9 +708,9 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double* __res
     xh[e] = static_cast<double>(hi);
     xl[e] = static_cast<double>(lo);
   }
-  ntt_forward<Lay, true>(xd, t, scr, twf, twf);
-  ntt_forward<Lay, false>(xh, t, scr, twf, twf);
-  ntt_forward<Lay, false>(xl, t, scr, twf, twf);
+  ntt_forward<Lay, true, false>(xd, t, scr, twf, twf);
+  ntt_forward<Lay, false, false>(xh, t, scr, twf, twf);
+  ntt_forward<Lay, false, false>(xl, t, scr, twf, twf);
   // N^-1 mod P, folded into the products
   double ninv = 1.0;
   {
@@ -587,8 +722,8 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double* __res
     xh[e] = reduce(mulmod(de, xh[e]));
     xl[e] = reduce(mulmod(de, xl[e]));
   }
-  ntt_inverse<Lay>(xh, t, scr, twi, twi);
-  ntt_inverse<Lay>(xl, t, scr, twi, twi);
+  ntt_inverse<Lay, false>(xh, t, scr, twi, twi);
+  ntt_inverse<Lay, false>(xl, t, scr, twi, twi);
   if (!active) return;
   for (int e = 0; e < E; e++) {
     const int j = t + T * e;
@@ -668,10 +803,12 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
                 p.ks_t * (1 << p.ks_basebit), KS_MAXROWS);
   dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (p.ks_t == 8 && p.ks_basebit == 2)
-    hipLaunchKernelGGL((keyswitch_kernel<32, 8, 2>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
-                       p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
-  else if (p.ks_t * (1 << p.ks_basebit) <= 32)
+  if (p.ks_t == 8 && p.ks_basebit == 2) {
+    dim3 g8(static_cast<unsigned>((B + KS8_WAVES * KS8_CB - 1) / (KS8_WAVES * KS8_CB)),
+            static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
+    hipLaunchKernelGGL(keyswitch_t8b2_kernel, g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
+                       bits, gate_begin);
+  } else if (p.ks_t * (1 << p.ks_basebit) <= 32)
     hipLaunchKernelGGL((keyswitch_kernel<32, 0, 0>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
                        p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   else
