@@ -295,12 +295,19 @@ template <int LOGN>
 struct BrCfg {
   using Lay = Layout<LOGN>;
   static constexpr int N = Lay::N, E = Lay::E, T = Lay::T;
-  static constexpr int CPB = 256 / T;                // ciphertexts per block
+  // ciphertexts per block: a block's barriers couple the waves of all its
+  // ciphertexts, so fewer per block means less waiting on the slowest wave
+#ifdef GT_BR_CPB
+  static constexpr int CPB = GT_BR_CPB;
+#else
+  static constexpr int CPB = T >= 256 ? 1 : 256 / T;
+#endif
+  static constexpr int THREADS = CPB * T;
   static constexpr bool kTwLds = true;               // twiddle tables in LDS
 };
 
 template <int LOGN>
-__global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
+__global__ __launch_bounds__(BrCfg<LOGN>::THREADS, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
     const double* __restrict__ bk, const double* __restrict__ tw_fwd_g,
     const double* __restrict__ tw_inv_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
@@ -321,7 +328,7 @@ __global__ __launch_bounds__(256, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel
   const double* twf;
   const double* twi;
   if constexpr (C::kTwLds) {
-    for (int k = threadIdx.x; k < N; k += 256) {
+    for (int k = threadIdx.x; k < N; k += C::THREADS) {
       const int slot = tw_lds_slot<Lay>(k);
       s_tw[slot] = tw_fwd_g[k];
       s_tw[N + slot] = tw_inv_g[k];
@@ -742,7 +749,7 @@ int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* test
               hipStream_t st) {
   using C = BrCfg<LOGN>;
   const int64_t blocks = (B + C::CPB - 1) / C::CPB;
-  hipLaunchKernelGGL(blind_rotate_kernel<LOGN>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
+  hipLaunchKernelGGL(blind_rotate_kernel<LOGN>, dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st,
                      ek->bk_ntt, ek->tw_fwd, ek->tw_inv, ws.abar, testvec, ws.extract, ek->p.n,
                      ek->p.l, ek->p.bg_bit, B);
   return launch_status("blind_rotate_kernel");
