@@ -31,30 +31,33 @@ PEAK_LANE_OPS = 256 * 64 * 2.4e9
 PEAK_HBM = 8.0e12
 
 
-def algorithmic_lane_ops(p) -> float:
+def algorithmic_lane_ops(p, parts: int) -> float:
     """VALU lane-operations one bootstrap's blind rotation needs with the
-    exact fp64 transform (FMA = 1 op); address arithmetic, memory traffic and
-    loop control are not counted."""
-    N, n, l = p["N"], p["n"], p["l"]
-    bfly = N // 2 * int(math.log2(N))
-    fwd = 2 * l * bfly * 8                 # modmul (6) + add + sub per butterfly
-    pointwise = 2 * l * 4 * N * 7          # modmul + accumulate, 4 outputs
-    inv = 4 * (bfly * 8 + 2 * N * 3)       # butterflies + reduction before and after
-    decomp = 2 * N * 3 + 2 * l * N * 4     # rotation difference; digit extract + convert
-    combine = 2 * N * 11                   # two low-32 conversions, shift-add, accumulate
-    return float(n * (fwd + pointwise + inv + decomp + combine))
+    complex fp64 transform over n = N/2 points (FMA = 1 op; key split into
+    `parts` parts, so 2*parts transform-domain outputs); address arithmetic,
+    memory traffic and loop control are not counted."""
+    N, n_lwe, l = p["N"], p["n"], p["l"]
+    n = N // 2
+    outs = 2 * parts
+    bfly = n // 2 * int(math.log2(n))
+    fwd = 2 * l * bfly * 8                 # complex multiply (4) + 2 complex adds (4)
+    digits = 2 * l * N * 4 + 2 * N * 3     # digit extract + convert; rotation difference
+    pointwise = 2 * l * outs * n * 4       # complex multiply-accumulate: 4 FMAs
+    inv = outs * bfly * 8
+    convert = 2 * N * 2 * parts            # round (1 add) and shift-add per part, accumulate
+    return float(n_lwe * (fwd + digits + pointwise + inv + convert))
 
 
-def algorithmic_bytes_br(p, B) -> float:
+def algorithmic_bytes_br(p, B, parts) -> float:
     """Bytes the blind-rotation launch must move: the transform-domain key once,
     modulus-switched inputs in, extracted samples out."""
-    bk = p["n"] * 2 * p["l"] * 4 * p["N"] * 8
+    bk = p["n"] * 2 * p["l"] * 2 * parts * (p["N"] // 2) * 16
     return float(bk + B * (p["n"] + 1) * 2 + B * (p["N"] + 1) * 4)
 
 
 def kernel_source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("gt_kernels.hip", "gt_layout.hpp", "gt_modp.hpp"):
+    for f in ("gt_kernels.hip", "gt_layout.hpp"):
         with open(os.path.join(ROOT, "paper_1911_07101_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -164,7 +167,8 @@ def main():
 
     br_ms, br_n = stages["blind_rotate"]
     br_s = br_ms / 1e3 / max(br_n, 1)
-    ops = algorithmic_lane_ops(p) * B
+    parts, bound = tfhe.tfhe_transform_error_bound(p)
+    ops = algorithmic_lane_ops(p, parts) * B
     achieved = ops / br_s
     digest = kernel_source_digest()
     traffic = measured_traffic(digest)
@@ -191,17 +195,18 @@ def main():
             "unit": "T lane-op/s",
             "frac": achieved / PEAK_LANE_OPS,
             "traffic": traffic,
-            "ops_per_bootstrap": algorithmic_lane_ops(p),
+            "ops_per_bootstrap": algorithmic_lane_ops(p, parts),
             "launch_ms": br_s * 1e3,
         },
         "hbm": {
             "kernel": "blind_rotate_kernel",
-            "algorithmic_bytes_per_launch": algorithmic_bytes_br(p, B),
-            "achieved_GBps": algorithmic_bytes_br(p, B) / br_s / 1e9,
+            "algorithmic_bytes_per_launch": algorithmic_bytes_br(p, B, parts),
+            "achieved_GBps": algorithmic_bytes_br(p, B, parts) / br_s / 1e9,
             "peak_GBps": PEAK_HBM / 1e9,
         },
         "stage_ms_per_step": {k: (v[0] / max(v[1], 1)) for k, v in stages.items()},
         "truth_table_ok": truth_ok,
+        "transform": {"key_parts": parts, "worst_case_error": bound},
         "kernel_source_digest": digest,
         "device": torch.cuda.get_device_name(0),
     }

@@ -48,11 +48,13 @@ enum {
 
 /* TFHE parameters with k = 1 (one mask polynomial).
  * Supported: N in {256, 512, 1024, 2048}; 1 <= n <= 4096; 2 <= bg_bit,
- * l * bg_bit <= 32 and 2l * N * 2^(bg_bit-1) <= 2^22 (every coefficient of a
- * product of digits by a 16-bit half of the key then stays within 2^37, which
- * the NTT prime resolves exactly); ks_t * ks_basebit <= 32 and
- * ks_t * 2^ks_basebit <= 64 (the key rows of one coefficient fit the key-switch
- * kernel's LDS stage). */
+ * l * bg_bit <= 32; ks_t * ks_basebit <= 32 and ks_t * 2^ks_basebit <= 64 (the
+ * key rows of one coefficient fit the key-switch kernel's LDS stage).  The
+ * ring products are computed with a floating-point transform and rounded;
+ * the parameters must keep its worst-case error below 1/8 with the key split
+ * into 16-bit or 11-bit signed parts (it holds for all the parameter sets
+ * the library is tested on; it fails for example at N = 2048 with
+ * bg_bit = 16); otherwise key generation returns TFHE_EUNSUPPORTED. */
 typedef struct {
   int32_t n;          /* LWE dimension */
   int32_t N;          /* TRLWE ring degree */
@@ -100,6 +102,15 @@ int tfhe_keygen_from_seed(const tfhe_params* params, uint64_t seed, int device,
 int tfhe_secret_keygen(const tfhe_params* params, uint64_t seed, tfhe_secret_key** sk_out);
 int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** ek_out);
 void tfhe_secret_key_free(tfhe_secret_key* sk);
+
+/* Exactness of the ring products (host only, no device needed).  The blind
+ * rotation multiplies digit polynomials by the key in a floating-point
+ * transform and rounds the results; the key's coefficients are split into
+ * `*key_parts` signed parts (2 of 16 bits or 3 of 11 bits) so that the
+ * worst-case transform error of every output coefficient, `*error_bound`,
+ * stays below 1/8 (the rounding then returns the exact integer).  Returns
+ * TFHE_EUNSUPPORTED (with the 3-part bound) when no split achieves it. */
+int tfhe_transform_error_bound(const tfhe_params* params, int32_t* key_parts, double* error_bound);
 void tfhe_eval_key_free(tfhe_eval_key* ek);
 int tfhe_eval_key_params(const tfhe_eval_key* ek, tfhe_params* out);
 

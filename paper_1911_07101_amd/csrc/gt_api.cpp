@@ -32,10 +32,11 @@ int check_params(const tfhe_params& p) {
   if (p.l < 1 || p.bg_bit < 2 || p.l * p.bg_bit > 32)
     return fail(TFHE_EUNSUPPORTED, "gadget l=%d bg_bit=%d: need bg_bit >= 2 and l*bg_bit <= 32", p.l,
                 p.bg_bit);
-  // every coefficient of sum_r digit_r * half_r must stay within 2^37 < P/2 - 2^37
-  const double bound = 2.0 * p.l * p.N * static_cast<double>(1u << (p.bg_bit - 1));
-  if (bound > 4194304.0)
-    return fail(TFHE_EUNSUPPORTED, "2l*N*Bg/2 = %.0f exceeds 2^22 (exactness bound of the transform)", bound);
+  // the fp64 transform must reproduce every product exactly after rounding
+  if (key_parts(p) == 0)
+    return fail(TFHE_EUNSUPPORTED,
+                "l=%d bg_bit=%d N=%d: the transform error bound exceeds 1/8 even with 11-bit key parts",
+                p.l, p.bg_bit, p.N);
   if (p.ks_basebit < 1 || p.ks_basebit > 6 || p.ks_t < 1 || p.ks_t * p.ks_basebit > 32 ||
       p.ks_t * (1 << p.ks_basebit) > 64)
     return fail(TFHE_EUNSUPPORTED,
@@ -191,21 +192,24 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   if (!ek) return fail(TFHE_ENOMEM, "host allocation failed");
   ek->p = p;
   ek->device = device;
-  ek->bk_ntt = nullptr;
-  ek->tw_fwd = ek->tw_inv = nullptr;
+  ek->parts = key_parts(p);
+  ek->bk_fft = nullptr;
+  ek->tw = nullptr;
   ek->ksk = nullptr;
-  ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 4 * p.N * 8;
+  // [n][2l][2 * parts][N/2] complex doubles
+  ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
   ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
+  const int64_t tw_bytes = static_cast<int64_t>(p.N / 2) * 16;
 
-  std::vector<double> bk_host, tw(2 * static_cast<size_t>(p.N));
+  std::vector<double> bk_host, tw(static_cast<size_t>(p.N));
   try {
     bk_host.resize(static_cast<size_t>(ek->bk_bytes / 8));
   } catch (const std::bad_alloc&) {
     delete ek;
     return fail(TFHE_ENOMEM, "host allocation failed for the transform-domain key");
   }
-  bk_to_transform_host(p, sk->bk.data(), bk_host.data());
-  twiddles_host(p.N, tw.data(), tw.data() + p.N);
+  bk_to_transform_host(p, ek->parts, sk->bk.data(), bk_host.data());
+  twiddles_host(p.N, tw.data());
 
   int rc = TFHE_OK;
   hipError_t e;
@@ -214,12 +218,11 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
     rc = fail(TFHE_EDEVICE, "cannot select device %d", device);
     goto fail_out;
   }
-  if ((e = hipMalloc(&ek->bk_ntt, ek->bk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(bk): %s", hipGetErrorString(e)); goto fail_out; }
-  if ((e = hipMalloc(&ek->tw_fwd, 2 * sizeof(double) * p.N)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(twiddles): %s", hipGetErrorString(e)); goto fail_out; }
-  ek->tw_inv = ek->tw_fwd + p.N;
+  if ((e = hipMalloc(&ek->bk_fft, ek->bk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(bk): %s", hipGetErrorString(e)); goto fail_out; }
+  if ((e = hipMalloc(&ek->tw, tw_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(twiddles): %s", hipGetErrorString(e)); goto fail_out; }
   if ((e = hipMalloc(&ek->ksk, ek->ksk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(ksk): %s", hipGetErrorString(e)); goto fail_out; }
-  if ((e = hipMemcpy(ek->bk_ntt, bk_host.data(), ek->bk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy bk"); goto fail_out; }
-  if ((e = hipMemcpy(ek->tw_fwd, tw.data(), 2 * sizeof(double) * p.N, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy twiddles"); goto fail_out; }
+  if ((e = hipMemcpy(ek->bk_fft, bk_host.data(), ek->bk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy bk"); goto fail_out; }
+  if ((e = hipMemcpy(ek->tw, tw.data(), tw_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy twiddles"); goto fail_out; }
   if ((e = hipMemcpy(ek->ksk, sk->ksk.data(), ek->ksk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy ksk"); goto fail_out; }
   *ek_out = ek;
   return TFHE_OK;
@@ -249,11 +252,22 @@ int tfhe_keygen_from_seed(const tfhe_params* params, uint64_t seed, int device,
 
 void tfhe_secret_key_free(tfhe_secret_key* sk) { delete sk; }
 
+int tfhe_transform_error_bound(const tfhe_params* params, int32_t* parts_out, double* error_bound) {
+  if (!params || !parts_out || !error_bound) return fail(TFHE_EINVAL, "NULL argument");
+  if (params->N < 256 || params->N > 2048 || (params->N & (params->N - 1)) || params->l < 1 ||
+      params->bg_bit < 2 || params->bg_bit > 30)
+    return fail(TFHE_EUNSUPPORTED, "N, l or bg_bit out of range");
+  const int parts = key_parts(*params);
+  *parts_out = parts ? parts : 3;
+  *error_bound = transform_error_bound(*params, *parts_out);
+  return parts ? TFHE_OK : fail(TFHE_EUNSUPPORTED, "error bound %.3g exceeds 1/8", *error_bound);
+}
+
 void tfhe_eval_key_free(tfhe_eval_key* ek) {
   if (!ek) return;
   DeviceGuard g(ek->device);
-  if (ek->bk_ntt) (void)hipFree(ek->bk_ntt);
-  if (ek->tw_fwd) (void)hipFree(ek->tw_fwd);
+  if (ek->bk_fft) (void)hipFree(ek->bk_fft);
+  if (ek->tw) (void)hipFree(ek->tw);
   if (ek->ksk) (void)hipFree(ek->ksk);
   delete ek;
 }

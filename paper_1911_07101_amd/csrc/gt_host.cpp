@@ -7,6 +7,7 @@
 // function of the seed.
 #include <algorithm>
 #include <cmath>
+#include <cstdint>
 #include <cstring>
 #include <thread>
 #include <vector>
@@ -173,124 +174,180 @@ void encrypt_host(const tfhe_secret_key& sk, uint64_t seed, const uint32_t* mu, 
 }
 
 // ------------------------------------------------- transform-domain key
-// Exact integer arithmetic mod P on the host (128-bit products); the device
-// reaches the same residues with its fp64 error-free arithmetic.
+// The ring product is computed as a complex transform of the folded
+// polynomial z_j = a_j + i a_{j+n} (n = N/2) over C[X]/(X^n - i): R[X]/(X^N+1)
+// and C[X]/(X^n - i) are isomorphic as real algebras (X^n = i is a square
+// root of X^N = -1), and z evaluated at the n roots of X^n - i gives a at
+// those roots.  The Cooley-Tukey tree splits node k, X^m - zeta^R(k) with
+// zeta = exp(i pi / N), into X^(m/2) -/+ zeta^(R(k)/2); R(1) = n and, since
+// -1 = zeta^N, R(2k) = R(k)/2, R(2k+1) = R(k)/2 + N.  The butterfly of node k
+// multiplies by tw[k] = zeta^(R(k)/2).
+//
+// The host builds the twiddles and the transformed key in long double and
+// rounds once to double.
 namespace {
 
-constexpr uint64_t kPrimeU = 549755731969ull;  // the NTT prime (see gt_modp.hpp)
-
-inline uint64_t mulmod_u64(uint64_t a, uint64_t b) {
-  return static_cast<uint64_t>((static_cast<unsigned __int128>(a) * b) % kPrimeU);
-}
-inline uint64_t powmod_u64(uint64_t a, uint64_t e) {
-  uint64_t r = 1;
-  while (e) {
-    if (e & 1) r = mulmod_u64(r, a);
-    a = mulmod_u64(a, a);
-    e >>= 1;
-  }
-  return r;
-}
 inline int ilog2(int x) {
   int r = 0;
   while ((1 << r) < x) r++;
   return r;
 }
-inline uint32_t bitrev(uint32_t x, int bits) {
-  uint32_t r = 0;
-  for (int b = 0; b < bits; b++) r |= ((x >> b) & 1u) << (bits - 1 - b);
-  return r;
-}
-// psi: a primitive 2N-th root of unity.  7 is a quadratic non-residue mod P,
-// so 7^((P-1)/2N) has order exactly 2N.
-uint64_t root_2n(int N) { return powmod_u64(7, (kPrimeU - 1) / (2 * static_cast<uint64_t>(N))); }
 
-struct TwiddleTable {
-  std::vector<uint64_t> fwd;  // psi^brv(k)
-  std::vector<uint64_t> inv;  // psi^-brv(k)
-  explicit TwiddleTable(int N) : fwd(N), inv(N) {
-    const int logn = ilog2(N);
-    const uint64_t psi = root_2n(N);
-    const uint64_t psi_inv = powmod_u64(psi, kPrimeU - 2);
-    for (int k = 0; k < N; k++) {
-      fwd[k] = powmod_u64(psi, bitrev(k, logn));
-      inv[k] = powmod_u64(psi_inv, bitrev(k, logn));
-    }
+// exponents e(k) = R(k)/2 of the twiddles, k in [1, n)
+std::vector<long> twiddle_exponents(int N) {
+  const int n = N / 2;
+  std::vector<long> R(2 * static_cast<size_t>(n), 0), e(n, 0);
+  R[1] = n;
+  for (int k = 1; k < n; k++) {
+    R[2 * k] = R[k] / 2;
+    R[2 * k + 1] = R[k] / 2 + N;
   }
+  for (int k = 1; k < n; k++) e[k] = R[k] / 2;
+  return e;
+}
+
+struct ComplexL {
+  long double re, im;
 };
 
-// in-place forward negacyclic NTT (Cooley-Tukey, natural order in,
-// bit-reversed order out); x holds residues in [0, P)
-void ntt_forward_u64(std::vector<uint64_t>& x, const TwiddleTable& tw) {
-  const int N = static_cast<int>(x.size());
+std::vector<ComplexL> twiddles_long(int N) {
+  const int n = N / 2;
+  const std::vector<long> ex = twiddle_exponents(N);
+  const long double pi = 3.141592653589793238462643383279502884L;
+  std::vector<ComplexL> tw(n);
+  tw[0] = {1.0L, 0.0L};
+  for (int k = 1; k < n; k++) {
+    const long double ang = pi * static_cast<long double>(ex[k]) / static_cast<long double>(N);
+    tw[k] = {cosl(ang), sinl(ang)};
+  }
+  return tw;
+}
+
+// in-place forward transform (Cooley-Tukey, natural order in, tree order out)
+void transform_forward_long(std::vector<ComplexL>& x, const std::vector<ComplexL>& tw) {
+  const int n = static_cast<int>(x.size());
   int k = 1;
-  for (int len = N / 2; len >= 1; len >>= 1) {
-    for (int start = 0; start < N; start += 2 * len, k++) {
-      const uint64_t z = tw.fwd[k];
+  for (int len = n / 2; len >= 1; len >>= 1) {
+    for (int start = 0; start < n; start += 2 * len, k++) {
+      const ComplexL w = tw[k];
       for (int j = start; j < start + len; j++) {
-        const uint64_t t = mulmod_u64(z, x[j + len]);
-        x[j + len] = (x[j] + kPrimeU - t) % kPrimeU;
-        x[j] = (x[j] + t) % kPrimeU;
+        const ComplexL v = x[j + len];
+        const ComplexL t = {w.re * v.re - w.im * v.im, w.re * v.im + w.im * v.re};
+        x[j + len] = {x[j].re - t.re, x[j].im - t.im};
+        x[j] = {x[j].re + t.re, x[j].im + t.im};
       }
     }
+  }
+}
+
+// split a signed 32-bit coefficient into `parts` signed pieces of
+// 32/parts-bit weight: value = sum_s piece_s * 2^(s * shift)
+void split_coefficient(int32_t v, int parts, int64_t* piece) {
+  const int shift = key_part_shift(parts);
+  int64_t rest = v;
+  for (int s = 0; s < parts; s++) {
+    if (s == parts - 1) {
+      piece[s] = rest;
+      break;
+    }
+    const int64_t half = int64_t{1} << (shift - 1);
+    const int64_t mask = (int64_t{1} << shift) - 1;
+    const int64_t low = ((rest + half) & mask) - half;
+    piece[s] = low;
+    rest = (rest - low) >> shift;
   }
 }
 
 struct BkCtx {
   const tfhe_params* p;
+  int parts;
   const uint32_t* bk;
   double* out;
-  const TwiddleTable* tw;
+  const std::vector<ComplexL>* tw;
 };
 
 void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
   const BkCtx& c = *static_cast<BkCtx*>(vctx);
-  const int N = c.p->N;
-  const int logn = ilog2(N);
-  const int loge = log_values_per_thread(logn);
-  const int E = 1 << loge, T = N >> loge;
-  const uint64_t ninv = powmod_u64(static_cast<uint64_t>(N), kPrimeU - 2);
-  std::vector<uint64_t> hi(N), lo(N);
+  const int N = c.p->N, n = N / 2;
+  const int E = 1 << kRingLogE, T = n >> kRingLogE;
+  const int S = c.parts;
+  std::vector<std::vector<ComplexL>> z(S, std::vector<ComplexL>(n));
+  int64_t piece_lo[4], piece_hi[4];
   for (int64_t row = begin; row < end; row++) {  // row = (i * 2l + r) * 2 + q
     const uint32_t* src = c.bk + row * N;
-    for (int m = 0; m < N; m++) {
-      // signed 16-bit halves: coefficient = hi * 2^16 + lo, lo in [-2^15, 2^15)
-      const int64_t sv = static_cast<int32_t>(src[m]);
-      const int64_t l16 = ((sv + 32768) & 0xFFFF) - 32768;
-      const int64_t h16 = (sv - l16) / 65536;
-      hi[m] = static_cast<uint64_t>((h16 + static_cast<int64_t>(kPrimeU)) % static_cast<int64_t>(kPrimeU));
-      lo[m] = static_cast<uint64_t>((l16 + static_cast<int64_t>(kPrimeU)) % static_cast<int64_t>(kPrimeU));
+    for (int j = 0; j < n; j++) {
+      split_coefficient(static_cast<int32_t>(src[j]), S, piece_lo);
+      split_coefficient(static_cast<int32_t>(src[j + n]), S, piece_hi);
+      for (int s = 0; s < S; s++)
+        z[s][j] = {static_cast<long double>(piece_lo[s]), static_cast<long double>(piece_hi[s])};
     }
-    ntt_forward_u64(hi, *c.tw);
-    ntt_forward_u64(lo, *c.tw);
-    // output slots o = 2q (high half), 2q + 1 (low half) of [i][r][o][e][t]
     const int64_t ir = row / 2, q = row % 2;
-    double* dst_hi = c.out + (ir * 4 + 2 * q) * N;
-    double* dst_lo = dst_hi + N;
-    // thread t's values e = 2h, 2h+1 are adjacent: layout [E/2][T][2]
-    for (int t = 0; t < T; t++)
-      for (int e = 0; e < E; e++) {
-        const int j = e | (t << loge);  // transform-domain index held by (t, e)
-        const int slot = (e >> 1) * 2 * T + 2 * t + (e & 1);
-        dst_hi[slot] = static_cast<double>(mulmod_u64(hi[j], ninv));
-        dst_lo[slot] = static_cast<double>(mulmod_u64(lo[j], ninv));
-      }
+    for (int s = 0; s < S; s++) {
+      transform_forward_long(z[s], *c.tw);
+      // output slot o = q * S + s of [i][r][o][e][t] (complex), scaled by 1/n
+      double* dst = c.out + ((ir * 2 * S + q * S + s) * static_cast<int64_t>(n)) * 2;
+      for (int t = 0; t < T; t++)
+        for (int e = 0; e < E; e++) {
+          const int j = e | (t << kRingLogE);  // point held by (t, e) after the forward transform
+          const int slot = e * T + t;
+          dst[2 * slot] = static_cast<double>(z[s][j].re / static_cast<long double>(n));
+          dst[2 * slot + 1] = static_cast<double>(z[s][j].im / static_cast<long double>(n));
+        }
+    }
   }
 }
 
 }  // namespace
 
-void bk_to_transform_host(const tfhe_params& p, const uint32_t* bk, double* out) {
-  TwiddleTable tw(p.N);
-  BkCtx ctx{&p, bk, out, &tw};
+int key_part_shift(int parts) { return parts == 2 ? 16 : 11; }
+
+int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
+
+// Worst-case error of one output coefficient of sum_{r<2l} digit_r * part_r
+// computed with the fp64 transform (forward transform of the digits on the
+// device, key transformed exactly and rounded once, pointwise products and
+// sums, inverse transform).  Radix-2 transform error (Higham, Accuracy and
+// Stability of Numerical Algorithms, Thm 24.2): ||fl(Fx) - Fx||_2 <=
+// m*eta/(1 - m*eta) ||Fx||_2 with eta = mu + gamma4 (sqrt2 + mu), m = log2 n,
+// mu the twiddle error (<= u after one rounding).  With x the folded digits and
+// y a key part (n points), R = 2l products:
+//   ||err||_inf <= R [eps ||x||_2 ||y||_1 + (eps + 3u) ||x||_1 ||y||_2
+//                     + 2u ||x||_1 ||y||_1] + eps ||z||_2
+// where ||x||_2 <= (Bg/2) sqrt(N), ||x||_1 <= (Bg/2) N, likewise for y with
+// the part bound 2^b, and ||z||_2 <= sqrt(N) R N (Bg/2) 2^b.
+double transform_error_bound(const tfhe_params& p, int parts) {
+  const double u = std::ldexp(1.0, -53);
+  const int n = p.N / 2;
+  const double m = ilog2(n);
+  const double gamma4 = 4 * u / (1 - 4 * u);
+  const double eta = u + gamma4 * (std::sqrt(2.0) + u);
+  const double eps = m * eta / (1 - m * eta);
+  const double R = 2.0 * p.l;
+  const double dig = std::ldexp(1.0, p.bg_bit - 1);
+  const double part = std::ldexp(1.0, key_part_bits(parts));
+  const double N = p.N, sN = std::sqrt(N);
+  const double x2 = dig * sN, x1 = dig * N, y2 = part * sN, y1 = part * N;
+  const double z2 = sN * R * N * dig * part;
+  return R * (eps * x2 * y1 + (eps + 3 * u) * x1 * y2 + 2 * u * x1 * y1) + eps * z2;
+}
+
+int key_parts(const tfhe_params& p) {
+  for (int parts = 2; parts <= 3; parts++)
+    if (transform_error_bound(p, parts) <= 0.125) return parts;
+  return 0;
+}
+
+void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out) {
+  const std::vector<ComplexL> tw = twiddles_long(p.N);
+  BkCtx ctx{&p, parts, bk, out, &tw};
   parallel_for(static_cast<int64_t>(p.n) * 2 * p.l * 2, 16, bk_convert_rows, &ctx);
 }
 
-void twiddles_host(int N, double* fwd, double* inv) {
-  TwiddleTable tw(N);
-  for (int k = 0; k < N; k++) {
-    fwd[k] = static_cast<double>(tw.fwd[k]);
-    inv[k] = static_cast<double>(tw.inv[k]);
+void twiddles_host(int N, double* tw) {
+  const std::vector<ComplexL> t = twiddles_long(N);
+  for (int k = 0; k < N / 2; k++) {
+    tw[2 * k] = static_cast<double>(t[k].re);
+    tw[2 * k + 1] = static_cast<double>(t[k].im);
   }
 }
 

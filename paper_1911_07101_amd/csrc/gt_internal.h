@@ -18,9 +18,9 @@ struct tfhe_secret_key {
 struct tfhe_eval_key {
   tfhe_params p;
   int device;
-  double* bk_ntt;   // device [n][2l][4][N] in transform-domain layout, times N^-1
-  double* tw_fwd;   // device [N]: psi^brv(k)
-  double* tw_inv;   // device [N]: psi^-brv(k)
+  int parts;        // the key's coefficients are split into 2 (16-bit) or 3 (11-bit) signed parts
+  double* bk_fft;   // device [n][2l][2*parts][N/2] complex (re, im), transform layout, times 2/N
+  double* tw;       // device [N/2] complex twiddles of the transform tree
   uint32_t* ksk;    // device [N][t][base-1][n+1]
   int64_t bk_bytes;
   int64_t ksk_bytes;
@@ -44,8 +44,12 @@ uint32_t rand_noise(uint64_t seed, uint32_t tag, uint64_t idx, double alpha);
 void keygen_host(tfhe_secret_key& sk);
 void encrypt_host(const tfhe_secret_key& sk, uint64_t seed, const uint32_t* mu, int64_t first,
                   int64_t count, uint32_t* ct);
-void bk_to_transform_host(const tfhe_params& p, const uint32_t* bk, double* out);
-void twiddles_host(int N, double* fwd, double* inv);
+int key_part_shift(int parts);
+int key_part_bits(int parts);
+double transform_error_bound(const tfhe_params& p, int parts);
+int key_parts(const tfhe_params& p);  // 2 or 3, 0 if no split keeps the bound
+void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out);
+void twiddles_host(int N, double* tw);
 void parallel_for(int64_t count, int64_t grain, void (*fn)(int64_t, int64_t, void*), void* ctx);
 
 // device launchers (gt_kernels.hip); return TFHE_OK or TFHE_EHIP

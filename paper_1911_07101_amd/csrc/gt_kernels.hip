@@ -2,29 +2,33 @@
 //
 //   prep_kernel          gate pre-combination (Section 3.1 gates; NOT is free)
 //                        and modulus switch of every LWE word to Z_{2N}
-//   blind_rotate_kernel  accumulator init, n CMux external products with exact
-//                        negacyclic products (fp64 NTT mod P), SampleExtract
+//   blind_rotate_kernel  accumulator init, n CMux external products, SampleExtract
 //   keyswitch_kernel     LWE key switching back to dimension n
 //   relu_sign_kernel     trivial 0 for the sign bit of the ReLU output
 //   not_kernel           NOT without bootstrapping
-//   negacyclic_mul_kernel  standalone exact product (checks the transform)
+//   negacyclic_mul_kernel  standalone ring product (checks the transform)
 //
-// Blind rotation layout: one polynomial of a ciphertext is held by T = N/E
-// threads with E values each (gt_layout.hpp); T = 64 (one wave) for
-// N <= 1024 and 128 for N = 2048.  A 256-thread block carries 256/T
-// ciphertexts.  The accumulator (two u32 polynomials) and a transpose scratch
-// of N doubles per ciphertext live in LDS; the four transform-domain
-// accumulators of an external product (mask/body x high/low key halves) live
-// in registers.  The bootstrapping key is read straight from global memory in
-// the transform-domain layout, coalesced across the T threads, and shared by
-// all ciphertexts in flight through L2.
+// The external product's negacyclic products are computed with a complex
+// fp64 transform of the folded polynomial (N/2 points) and rounded back to
+// integers; the key is split into signed parts small enough that the
+// transform's worst-case error stays below 1/8, so the rounded result equals
+// the exact product (bound in gt_host.cpp, transform_error_bound).
+//
+// Blind rotation layout: a ciphertext's transforms are held by T = N/8
+// threads with 4 complex points each (gt_layout.hpp): T = 128 (two waves) at
+// N = 1024, 256 at N = 2048.  The accumulator (two u32 polynomials), a
+// transpose scratch of N/2 complex points per ciphertext and a copy of the
+// twiddle table live in LDS; the transform-domain accumulators of an external
+// product ((mask, body) x key parts) live in registers.  The bootstrapping key
+// is read from global memory in the transform-domain layout, one 16-byte
+// point per load, coalesced across the T threads and shared by all
+// ciphertexts in flight through L2.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
 
 #include "gt_internal.h"
 #include "gt_layout.hpp"
-#include "gt_modp.hpp"
 
 namespace gt {
 
@@ -46,10 +50,34 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
+// ----------------------------------------------------------- complex fp64
+__device__ __forceinline__ double2 cmul(double2 a, double2 w) {
+  return make_double2(fma(a.x, w.x, -(a.y * w.y)), fma(a.x, w.y, a.y * w.x));
+}
+__device__ __forceinline__ double2 cmul_conj(double2 a, double2 w) {  // a * conj(w)
+  return make_double2(fma(a.x, w.x, a.y * w.y), fma(a.y, w.x, -(a.x * w.y)));
+}
+__device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ void cmac(double2& acc, double2 a, double2 w) {
+  acc.x = fma(a.x, w.x, acc.x);
+  acc.x = fma(-a.y, w.y, acc.x);
+  acc.y = fma(a.x, w.y, acc.y);
+  acc.y = fma(a.y, w.x, acc.y);
+}
+
+// v is within 1/2 of an integer k with |k| < 2^51: adding 1.5 * 2^52 rounds it
+// to k + 1.5 * 2^52, whose mantissa field is k + 2^51, so the low 32 bits of
+// the double's bit pattern are k mod 2^32
+__device__ __forceinline__ uint32_t round_low32(double v) {
+  const double s = v + 6755399441055744.0;
+  return static_cast<uint32_t>(__double_as_longlong(s));
+}
+
 // Make LDS writes of all threads of a polynomial visible to its other threads.
-// A polynomial held by a single wave needs only ordering (a wave's LDS
-// operations complete in order); a polynomial spread over two waves needs the
-// block barrier.
+// A polynomial held by one wave needs only ordering (a wave's LDS operations
+// complete in order); a polynomial spread over several waves needs the block
+// barrier.
 template <int T>
 __device__ __forceinline__ void poly_sync() {
   if constexpr (T <= 64) {
@@ -61,17 +89,18 @@ __device__ __forceinline__ void poly_sync() {
   }
 }
 
-// bank swizzle of the transpose scratch: with 8 values per thread every pass
-// layout at N = 512..2048 reads and writes 64-bit elements without bank
-// conflicts (checked for 32 and 64 banks of 4 bytes); it permutes only the low
-// 5 bits, so it stays inside the polynomial
-__device__ __forceinline__ int swz(int j) { return j ^ (((j >> 3) ^ (j >> 7)) & 31); }
+// bank swizzle of the transpose scratch: with 4 complex (16-byte) points per
+// thread every pass layout at n = 128..1024 reads and writes without bank
+// conflicts (checked for 32 and 64 banks of 4 bytes); it permutes only the
+// low 4 bits, so it stays inside the polynomial
+__device__ __forceinline__ int swz(int j) { return j ^ (((j >> 1) ^ (j >> 2)) & 15); }
 
-// Position of twiddle k in the LDS copy of a twiddle table.  Stage s owns
-// k in [N/2^(s+1), N/2^s); in a pass other than the first, thread t reads the
+// Position of twiddle k in the LDS copy of the twiddle table.  Stage s owns
+// k in [n/2^(s+1), n/2^s); in a pass other than the first, thread t reads the
 // stage's entries m = (t >> w) * G + g, g < G, so they are stored [g][t >> w]
-// to make the threads of a wave read consecutive words.  First-pass twiddles
-// are read uniformly from global memory and keep their natural place.
+// to make the threads of a wave read consecutive entries.  First-pass
+// twiddles are the same for every thread, are read from global memory through
+// the scalar cache, and keep their natural place.
 template <class Lay>
 __host__ __device__ constexpr int tw_lds_slot(int k) {
   if (k == 0) return 0;
@@ -90,7 +119,7 @@ __host__ __device__ constexpr int tw_lds_slot(int k) {
 }
 
 template <class Lay, int WFROM, int WTO>
-__device__ __forceinline__ void transpose(double (&x)[Lay::E], int t, double* scr) {
+__device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* scr) {
   static_for<0, Lay::E>([&](auto EI) {
     constexpr int e = decltype(EI)::value;
     scr[swz(Lay::jmap(t, e, WFROM))] = x[e];
@@ -116,27 +145,24 @@ constexpr int tw_offset(int p, int k, bool fwd) {
   return off;
 }
 
-// Forward negacyclic NTT (Cooley-Tukey butterflies, twiddle psi^brv(k) for the
-// block of coefficient j at stage s: k = N/2^(s+1) + j/2^(s+1)).  In: pass-0
-// (coefficient) layout; out: last-pass (transform) layout.  |in| < 2^10 gives
-// |out| < 2^43 (each stage adds at most 0.75P + 2^35).  The twiddles of a pass
-// are fetched together before its butterflies: pass 0's are the same for every
-// thread (tw_uniform, read through the scalar cache), the others come from
-// tw: an LDS copy laid out by tw_lds_slot (TW_PERMUTED) or a natural-order
-// table in global memory.  SMALL_IN: inputs are below 2^10 in magnitude, so the first
-// stage's products are exact without the low part.
-template <class Lay, bool SMALL_IN, bool TW_PERMUTED>
-__device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* scr,
-                                            const double* __restrict__ tw,
-                                            const double* __restrict__ tw_uniform) {
+// Forward transform of the folded polynomial over C[X]/(X^n - i)
+// (Cooley-Tukey butterflies; the block of point j at stage s splits tree node
+// k = n/2^(s+1) + j/2^(s+1) and multiplies by tw[k]).  In: pass-0 (coefficient)
+// layout; out: last-pass (transform) layout.  The twiddles of a pass are
+// fetched together before its butterflies: pass 0's are the same for every
+// thread (tw_uniform, global memory), the others come from tw, an LDS copy
+// laid out by tw_lds_slot (TW_PERMUTED) or a natural-order table.
+template <class Lay, bool TW_PERMUTED>
+__device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2* scr,
+                                            const double2* __restrict__ tw,
+                                            const double2* __restrict__ tw_uniform) {
   constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
     if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w>(x, t, scr);
-    // twiddles of all stages of the pass: stage si uses z[off(si) .. off(si) + G(si))
-    double z[E];
+    double2 z[E];
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
       constexpr int b = s - w;
@@ -157,37 +183,34 @@ __device__ __forceinline__ void ntt_forward(double (&x)[Lay::E], int t, double* 
       constexpr int b = s - w;
       constexpr int G = E >> (b + 1);
       constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, true);
-      constexpr bool small = SMALL_IN && p == 0 && decltype(SI)::value == 0;
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
-          const double u = x[e];
-          const double v = small ? mulmod_small(x[e2], z[off + g]) : mulmod(x[e2], z[off + g]);
-          x[e] = u + v;
-          x[e2] = u - v;
+          const double2 u = x[e];
+          const double2 v = cmul(x[e2], z[off + g]);
+          x[e] = cadd(u, v);
+          x[e2] = csub(u, v);
         });
       });
     });
   });
 }
 
-// Inverse transform without the 1/N factor (Gentleman-Sande butterflies,
-// twiddle psi^-brv(k)).  In: transform layout, |in| <= P/2 + 1; out:
-// coefficient layout, |out| < 2^(38 + LOGN) (sums double per stage).
+// Inverse transform without the 1/n factor (Gentleman-Sande butterflies with
+// the conjugate twiddles).  In: transform layout; out: coefficient layout.
 template <class Lay, bool TW_PERMUTED>
-__device__ __forceinline__ void ntt_inverse(double (&x)[Lay::E], int t, double* scr,
-                                            const double* __restrict__ tw,
-                                            const double* __restrict__ tw_uniform) {
+__device__ __forceinline__ void fft_inverse(double2 (&x)[Lay::E], int t, double2* scr,
+                                            const double2* __restrict__ tw,
+                                            const double2* __restrict__ tw_uniform) {
   constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = Lay::NPASS - 1 - decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
     if constexpr (p < Lay::NPASS - 1) transpose<Lay, Lay::win(p + 1), w>(x, t, scr);
-    // stage si (ascending bit s = lo + si) uses z[off(si) .. off(si) + G(si))
-    double z[E];
+    double2 z[E];
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::lo(p) + decltype(SI)::value;
       constexpr int b = s - w;
@@ -213,10 +236,10 @@ __device__ __forceinline__ void ntt_inverse(double (&x)[Lay::E], int t, double* 
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
-          const double u = x[e];
-          const double v = x[e2];
-          x[e] = u + v;
-          x[e2] = mulmod(u - v, z[off + g]);
+          const double2 u = x[e];
+          const double2 v = x[e2];
+          x[e] = cadd(u, v);
+          x[e2] = cmul_conj(csub(u, v), z[off + g]);
         });
       });
     });
@@ -232,6 +255,7 @@ __device__ __forceinline__ uint32_t rot_coef(const uint32_t* p, uint32_t e, int 
   const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e / N) & 1u));
   return (v ^ m) - m;
 }
+
 
 // ------------------------------------------------------------ prep kernel
 __device__ __forceinline__ uint16_t mod_switch(uint32_t x, int N) {
@@ -291,33 +315,35 @@ __global__ __launch_bounds__(256) void prep_kernel(int mode, int gate, const uin
 }
 
 // ------------------------------------------------------ blind rotation
-template <int LOGN>
+// Ring degree 2^LOGN, key coefficients split into S signed parts.
+template <int LOGN, int S>
 struct BrCfg {
-  using Lay = Layout<LOGN>;
-  static constexpr int N = Lay::N, E = Lay::E, T = Lay::T;
-  // ciphertexts per block: a block's barriers couple the waves of all its
-  // ciphertexts, so fewer per block means less waiting on the slowest wave
+  using Lay = RingLayout<LOGN>;
+  static constexpr int NR = 1 << LOGN;  // ring degree
+  static constexpr int NC = Lay::N;     // complex points, NR / 2
+  static constexpr int E = Lay::E, T = Lay::T;
+  static constexpr int O = 2 * S;       // transform-domain accumulators: (mask, body) x parts
+  static constexpr int SHIFT = S == 2 ? 16 : 11;
+  // ciphertexts per block (two at T = 128: measured faster than one or four)
 #ifdef GT_BR_CPB
   static constexpr int CPB = GT_BR_CPB;
 #else
   static constexpr int CPB = T >= 256 ? 1 : 256 / T;
 #endif
   static constexpr int THREADS = CPB * T;
-  static constexpr bool kTwLds = true;               // twiddle tables in LDS
 };
 
-template <int LOGN>
-__global__ __launch_bounds__(BrCfg<LOGN>::THREADS, GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
-    const double* __restrict__ bk, const double* __restrict__ tw_fwd_g,
-    const double* __restrict__ tw_inv_g, const uint16_t* __restrict__ abar,
+template <int LOGN, int S>
+__global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
+    const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
     int64_t B) {
-  using C = BrCfg<LOGN>;
+  using C = BrCfg<LOGN, S>;
   using Lay = typename C::Lay;
-  constexpr int N = C::N, E = C::E, T = C::T, CPB = C::CPB;
-  __shared__ double s_tw[C::kTwLds ? 2 * N : 1];
-  __shared__ double s_scr[CPB * N];
-  __shared__ uint32_t s_acc[CPB * 2 * N];
+  constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
+  __shared__ double2 s_tw[NC];
+  __shared__ double2 s_scr[CPB * NC];
+  __shared__ uint32_t s_acc[CPB * 2 * NR];
 
   const int slot = threadIdx.x / T;
   const int t = threadIdx.x % T;
@@ -325,43 +351,33 @@ __global__ __launch_bounds__(BrCfg<LOGN>::THREADS, GT_BR_WAVES_PER_SIMD) void bl
   const bool active = c < B;
   if (!active) c = B - 1;  // idle slots repeat the last sample and write nothing
 
-  const double* twf;
-  const double* twi;
-  if constexpr (C::kTwLds) {
-    for (int k = threadIdx.x; k < N; k += C::THREADS) {
-      const int slot = tw_lds_slot<Lay>(k);
-      s_tw[slot] = tw_fwd_g[k];
-      s_tw[N + slot] = tw_inv_g[k];
-    }
-    __syncthreads();
-    twf = s_tw;
-    twi = s_tw + N;
-  } else {
-    twf = tw_fwd_g;
-    twi = tw_inv_g;
-  }
-  double* scr = s_scr + slot * N;
-  uint32_t* acc_a = s_acc + slot * 2 * N;
-  uint32_t* acc_b = acc_a + N;
+  for (int k = threadIdx.x; k < NC; k += C::THREADS) s_tw[tw_lds_slot<Lay>(k)] = tw_g[k];
+  __syncthreads();
+  double2* scr = s_scr + slot * NC;
+  uint32_t* acc_a = s_acc + slot * 2 * NR;
+  uint32_t* acc_b = acc_a + NR;
   const uint16_t* ab = abar + c * (n + 1);
 
-  // ACC = (0, X^{-bbar} v)
+  // ACC = (0, X^{-bbar} v); thread t owns ring coefficients t + T*e and t + T*e + NR/2
   {
     const uint32_t bbar = ab[n];
-    const uint32_t e0 = (2u * N - bbar) & (2u * N - 1);
-    for (int e = 0; e < E; e++) {
-      const int j = t + T * e;
-      acc_a[j] = 0u;
-      uint32_t v;
-      if (testvec == nullptr) {
-        const int src = j - static_cast<int>(e0 & (N - 1));
-        const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e0 / N) & 1u));
-        v = (kMu ^ m) - m;
-      } else {
-        v = rot_coef<N>(testvec, e0, j);
+    const uint32_t e0 = (2u * NR - bbar) & (2u * NR - 1);
+#pragma unroll
+    for (int e = 0; e < E; e++)
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const int j = t + T * e + h * NC;
+        acc_a[j] = 0u;
+        uint32_t v;
+        if (testvec == nullptr) {
+          const int src = j - static_cast<int>(e0 & (NR - 1));
+          const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e0 / NR) & 1u));
+          v = (kMu ^ m) - m;
+        } else {
+          v = rot_coef<NR>(testvec, e0, j);
+        }
+        acc_b[j] = v;
       }
-      acc_b[j] = v;
-    }
     poly_sync<T>();
   }
 
@@ -370,84 +386,94 @@ __global__ __launch_bounds__(BrCfg<LOGN>::THREADS, GT_BR_WAVES_PER_SIMD) void bl
   uint32_t offset = 0;
   for (int j = 1; j <= l; j++) offset += half << (32 - j * bg_bit);
   if (l * bg_bit < 32) offset += 1u << (31 - l * bg_bit);
-  const size_t bk_step = static_cast<size_t>(2 * l) * 4 * N;
+  const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;
 
   for (int i = 0; i < n; i++) {
     const uint32_t a_i = ab[i];
-    const double* bki = bk + static_cast<size_t>(i) * bk_step;
-    double acc[4][E];
+    const double2* bki = bk + static_cast<size_t>(i) * bk_step;
+    double2 acc[O][E];
 #pragma unroll
-    for (int o = 0; o < 4; o++)
+    for (int o = 0; o < O; o++)
 #pragma unroll
-      for (int e = 0; e < E; e++) acc[o][e] = 0.0;
+      for (int e = 0; e < E; e++) acc[o][e] = make_double2(0.0, 0.0);
 
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
-      uint32_t D[E];
+      // D = X^{a_i} P - P (plus the decomposition offset) at coefficients
+      // t + T*e (h = 0) and t + T*e + NR/2 (h = 1): point e's real and imaginary part
+      uint32_t D[2][E];
 #pragma unroll
-      for (int e = 0; e < E; e++) {
-        const int j = t + T * e;
-        D[e] = rot_coef<N>(P, a_i, j) - P[j] + offset;
-      }
+      for (int e = 0; e < E; e++)
+#pragma unroll
+        for (int h = 0; h < 2; h++) {
+          const int j = t + T * e + h * NC;
+          D[h][e] = rot_coef<NR>(P, a_i, j) - P[j] + offset;
+        }
       for (int jj = 0; jj < l; jj++) {
         const int shift = 32 - (jj + 1) * bg_bit;
-        double x[E];
+        double2 x[E];
 #pragma unroll
         for (int e = 0; e < E; e++)
-          x[e] = static_cast<double>(static_cast<int32_t>((D[e] >> shift) & dmask) - static_cast<int32_t>(half));
-        // key row r = q*l + jj: four output polynomials, each stored as
-        // [E/2][T][2] so a thread's pair of values is one 16-byte load
-        const double2* bkr =
-            reinterpret_cast<const double2*>(bki + static_cast<size_t>(q * l + jj) * 4 * N) + t;
-        ntt_forward<Lay, true, C::kTwLds>(x, t, scr, twf, tw_fwd_g);
-        double2 w[E / 2];
+          x[e] = make_double2(
+              static_cast<double>(static_cast<int32_t>((D[0][e] >> shift) & dmask) - static_cast<int32_t>(half)),
+              static_cast<double>(static_cast<int32_t>((D[1][e] >> shift) & dmask) - static_cast<int32_t>(half)));
+        fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
+        // key row r = q*l + jj: O outputs [o][e][t], one 16-byte point per load
+        const double2* bkr = bki + static_cast<size_t>(q * l + jj) * O * NC + t;
+        double2 w[E];
 #pragma unroll
-        for (int h = 0; h < E / 2; h++) w[h] = bkr[h * T];
+        for (int e = 0; e < E; e++) w[e] = bkr[e * T];
 #pragma unroll
-        for (int o = 0; o < 4; o++) {
-          double2 wn[E / 2];
-          if (o < 3) {
+        for (int o = 0; o < O; o++) {
+          double2 wn[E];
+          if (o + 1 < O) {
 #pragma unroll
-            for (int h = 0; h < E / 2; h++) wn[h] = bkr[(o + 1) * (N / 2) + h * T];
+            for (int e = 0; e < E; e++) wn[e] = bkr[((o + 1) * E + e) * T];
           }
 #pragma unroll
-          for (int h = 0; h < E / 2; h++) {
-            acc[o][2 * h] += mulmod(x[2 * h], w[h].x);
-            acc[o][2 * h + 1] += mulmod(x[2 * h + 1], w[h].y);
-          }
-          if (o < 3) {
+          for (int e = 0; e < E; e++) cmac(acc[o][e], x[e], w[e]);
+          if (o + 1 < O) {
 #pragma unroll
-            for (int h = 0; h < E / 2; h++) w[h] = wn[h];
+            for (int e = 0; e < E; e++) w[e] = wn[e];
           }
         }
       }
     }
 
 #pragma unroll
-    for (int o = 0; o < 4; o++) {
-#pragma unroll
-      for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
-      ntt_inverse<Lay, C::kTwLds>(acc[o], t, scr, twi, tw_inv_g);
-#pragma unroll
-      for (int e = 0; e < E; e++) acc[o][e] = reduce(acc[o][e]);
-    }
+    for (int o = 0; o < O; o++) fft_inverse<Lay, true>(acc[o], t, scr, s_tw, tw_g);
+    // every output is within 1/8 of an integer (the transform's error bound):
+    // round, take it mod 2^32 and recombine the key parts
 #pragma unroll
     for (int e = 0; e < E; e++) {
+      uint32_t ra0 = 0u, ra1 = 0u, rb0 = 0u, rb1 = 0u;
+#pragma unroll
+      for (int sp = S - 1; sp >= 0; sp--) {
+        ra0 = (ra0 << C::SHIFT) + round_low32(acc[sp][e].x);
+        ra1 = (ra1 << C::SHIFT) + round_low32(acc[sp][e].y);
+        rb0 = (rb0 << C::SHIFT) + round_low32(acc[S + sp][e].x);
+        rb1 = (rb1 << C::SHIFT) + round_low32(acc[S + sp][e].y);
+      }
       const int j = t + T * e;
-      acc_a[j] += (low32(acc[0][e]) << 16) + low32(acc[1][e]);
-      acc_b[j] += (low32(acc[2][e]) << 16) + low32(acc[3][e]);
+      acc_a[j] += ra0;
+      acc_a[j + NC] += ra1;
+      acc_b[j] += rb0;
+      acc_b[j + NC] += rb1;
     }
     poly_sync<T>();
   }
 
   // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0)
   if (active) {
-    uint32_t* out = extract + c * (N + 1);
-    for (int e = 0; e < E; e++) {
-      const int j = t + T * e;
-      out[j] = j == 0 ? acc_a[0] : 0u - acc_a[N - j];
-    }
-    if (t == 0) out[N] = acc_b[0];
+    uint32_t* out = extract + c * (NR + 1);
+#pragma unroll
+    for (int e = 0; e < E; e++)
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const int j = t + T * e + h * NC;
+        out[j] = j == 0 ? acc_a[0] : 0u - acc_a[NR - j];
+      }
+    if (t == 0) out[NR] = acc_b[0];
   }
 }
 
@@ -688,53 +714,67 @@ __global__ __launch_bounds__(256) void not_kernel(const uint32_t* __restrict__ i
   if (idx < words) out[idx] = 0u - in[idx];
 }
 
-// Standalone exact negacyclic product c = d * b in Z_{2^32}[X]/(X^N+1), one
-// polynomial per T threads, with the blind rotation's transform code.
-template <int LOGN>
-__global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double* __restrict__ twf,
-                                                             const double* __restrict__ twi,
+// Standalone negacyclic product c = d * b in Z_{2^32}[X]/(X^N+1) with the blind
+// rotation's transform code: d small signed digits, b split into S parts on
+// the device and transformed there.  One polynomial per T threads.
+template <int LOGN, int S>
+__global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double2* __restrict__ tw,
                                                              const int32_t* __restrict__ d,
                                                              const uint32_t* __restrict__ b,
                                                              uint32_t* __restrict__ c, int64_t B) {
-  using Lay = Layout<LOGN>;
-  constexpr int N = Lay::N, E = Lay::E, T = Lay::T, CPB = 256 / T;
-  __shared__ double s_scr[CPB * N];
+  using Lay = RingLayout<LOGN>;
+  constexpr int NR = 1 << LOGN, NC = Lay::N, E = Lay::E, T = Lay::T, CPB = 256 / T;
+  constexpr int SHIFT = S == 2 ? 16 : 11;
+  __shared__ double2 s_scr[CPB * NC];
   const int slot = threadIdx.x / T;
   const int t = threadIdx.x % T;
   int64_t k = static_cast<int64_t>(blockIdx.x) * CPB + slot;
   const bool active = k < B;
   if (!active) k = B - 1;
-  double* scr = s_scr + slot * N;
-  double xd[E], xh[E], xl[E];
+  double2* scr = s_scr + slot * NC;
+  double2 xd[E], xb[S][E];
+#pragma unroll
   for (int e = 0; e < E; e++) {
     const int j = t + T * e;
-    xd[e] = static_cast<double>(d[k * N + j]);
-    const int32_t sv = static_cast<int32_t>(b[k * N + j]);
-    const int32_t lo = ((sv + 32768) & 0xFFFF) - 32768;
-    const int32_t hi = static_cast<int32_t>((static_cast<int64_t>(sv) - lo) / 65536);
-    xh[e] = static_cast<double>(hi);
-    xl[e] = static_cast<double>(lo);
+    xd[e] = make_double2(static_cast<double>(d[k * NR + j]), static_cast<double>(d[k * NR + j + NC]));
+    int64_t rest0 = static_cast<int32_t>(b[k * NR + j]);
+    int64_t rest1 = static_cast<int32_t>(b[k * NR + j + NC]);
+#pragma unroll
+    for (int sp = 0; sp < S; sp++) {
+      int64_t p0 = rest0, p1 = rest1;
+      if (sp + 1 < S) {
+        const int64_t hb = int64_t{1} << (SHIFT - 1), mask = (int64_t{1} << SHIFT) - 1;
+        p0 = ((rest0 + hb) & mask) - hb;
+        p1 = ((rest1 + hb) & mask) - hb;
+        rest0 = (rest0 - p0) >> SHIFT;
+        rest1 = (rest1 - p1) >> SHIFT;
+      }
+      xb[sp][e] = make_double2(static_cast<double>(p0), static_cast<double>(p1));
+    }
   }
-  ntt_forward<Lay, true, false>(xd, t, scr, twf, twf);
-  ntt_forward<Lay, false, false>(xh, t, scr, twf, twf);
-  ntt_forward<Lay, false, false>(xl, t, scr, twf, twf);
-  // N^-1 mod P, folded into the products
-  double ninv = 1.0;
-  {
-    // P = 1 mod 2^14, so N^-1 = P - (P - 1) / N
-    ninv = kP - (kP - 1.0) / static_cast<double>(N);
+  fft_forward<Lay, false>(xd, t, scr, tw, tw);
+#pragma unroll
+  for (int sp = 0; sp < S; sp++) {
+    fft_forward<Lay, false>(xb[sp], t, scr, tw, tw);
+#pragma unroll
+    for (int e = 0; e < E; e++) {
+      const double2 pr = cmul(xd[e], xb[sp][e]);
+      xb[sp][e] = make_double2(pr.x / NC, pr.y / NC);  // exact: NC is a power of two
+    }
+    fft_inverse<Lay, false>(xb[sp], t, scr, tw, tw);
   }
-  for (int e = 0; e < E; e++) {
-    const double de = mulmod(xd[e], ninv);
-    xh[e] = reduce(mulmod(de, xh[e]));
-    xl[e] = reduce(mulmod(de, xl[e]));
-  }
-  ntt_inverse<Lay, false>(xh, t, scr, twi, twi);
-  ntt_inverse<Lay, false>(xl, t, scr, twi, twi);
   if (!active) return;
+#pragma unroll
   for (int e = 0; e < E; e++) {
+    uint32_t r0 = 0u, r1 = 0u;
+#pragma unroll
+    for (int sp = S - 1; sp >= 0; sp--) {
+      r0 = (r0 << SHIFT) + round_low32(xb[sp][e].x);
+      r1 = (r1 << SHIFT) + round_low32(xb[sp][e].y);
+    }
     const int j = t + T * e;
-    c[k * N + j] = (low32(reduce(xh[e])) << 16) + low32(reduce(xl[e]));
+    c[k * NR + j] = r0;
+    c[k * NR + j + NC] = r1;
   }
 }
 
@@ -744,26 +784,51 @@ inline int launch_status(const char* what) {
   return TFHE_OK;
 }
 
-template <int LOGN>
+template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
               hipStream_t st) {
-  using C = BrCfg<LOGN>;
+  using C = BrCfg<LOGN, S>;
   const int64_t blocks = (B + C::CPB - 1) / C::CPB;
-  hipLaunchKernelGGL(blind_rotate_kernel<LOGN>, dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st,
-                     ek->bk_ntt, ek->tw_fwd, ek->tw_inv, ws.abar, testvec, ws.extract, ek->p.n,
-                     ek->p.l, ek->p.bg_bit, B);
+  hipLaunchKernelGGL((blind_rotate_kernel<LOGN, S>), dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0,
+                     st, reinterpret_cast<const double2*>(ek->bk_fft), reinterpret_cast<const double2*>(ek->tw),
+                     ws.abar, testvec, ws.extract, ek->p.n, ek->p.l, ek->p.bg_bit, B);
   return launch_status("blind_rotate_kernel");
 }
 
-template <int LOGN>
+template <int LOGN, int S>
 int launch_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c, int64_t B,
                hipStream_t st) {
-  constexpr int CPB = 256 / Layout<LOGN>::T;
+  constexpr int CPB = 256 / RingLayout<LOGN>::T;
   const int64_t blocks = (B + CPB - 1) / CPB;
-  hipLaunchKernelGGL(negacyclic_mul_kernel<LOGN>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
-                     ek->tw_fwd, ek->tw_inv, d, b, c, B);
+  hipLaunchKernelGGL((negacyclic_mul_kernel<LOGN, S>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
+                     reinterpret_cast<const double2*>(ek->tw), d, b, c, B);
   return launch_status("negacyclic_mul_kernel");
 }
+
+template <template <int, int> class F, class... A>
+int dispatch_ring(const tfhe_eval_key* ek, A... args) {
+  const int N = ek->p.N, S = ek->parts;
+#define GT_CASE(LOGN, SP) \
+  if (N == (1 << LOGN) && S == SP) return F<LOGN, SP>::run(ek, args...);
+  GT_CASE(8, 2) GT_CASE(8, 3) GT_CASE(9, 2) GT_CASE(9, 3) GT_CASE(10, 2) GT_CASE(10, 3) GT_CASE(11, 2)
+  GT_CASE(11, 3)
+#undef GT_CASE
+  return fail(TFHE_EUNSUPPORTED, "no kernel for N=%d with %d key parts", N, S);
+}
+
+template <int LOGN, int S>
+struct BrRun {
+  static int run(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* tv, int64_t B, hipStream_t st) {
+    return launch_br<LOGN, S>(ek, ws, tv, B, st);
+  }
+};
+template <int LOGN, int S>
+struct MulRun {
+  static int run(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c, int64_t B,
+                 hipStream_t st) {
+    return launch_mul<LOGN, S>(ek, d, b, c, B, st);
+  }
+};
 
 }  // namespace
 
@@ -792,14 +857,7 @@ int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws,
 
 int launch_blind_rotate(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec,
                         int64_t B, void* stream) {
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  switch (ek->p.N) {
-    case 256: return launch_br<8>(ek, ws, testvec, B, st);
-    case 512: return launch_br<9>(ek, ws, testvec, B, st);
-    case 1024: return launch_br<10>(ek, ws, testvec, B, st);
-    case 2048: return launch_br<11>(ek, ws, testvec, B, st);
-    default: return fail(TFHE_EUNSUPPORTED, "N=%d has no blind-rotation kernel", ek->p.N);
-  }
+  return dispatch_ring<BrRun>(ek, ws, testvec, B, static_cast<hipStream_t>(stream));
 }
 
 int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B, int mode,
@@ -844,14 +902,7 @@ int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, vo
 
 int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c,
                           int64_t B, void* stream) {
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  switch (ek->p.N) {
-    case 256: return launch_mul<8>(ek, d, b, c, B, st);
-    case 512: return launch_mul<9>(ek, d, b, c, B, st);
-    case 1024: return launch_mul<10>(ek, d, b, c, B, st);
-    case 2048: return launch_mul<11>(ek, d, b, c, B, st);
-    default: return fail(TFHE_EUNSUPPORTED, "N=%d has no product kernel", ek->p.N);
-  }
+  return dispatch_ring<MulRun>(ek, d, b, c, B, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace gt

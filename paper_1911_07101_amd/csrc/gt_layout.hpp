@@ -1,15 +1,16 @@
-// Register/LDS layout of one polynomial inside the blind-rotation kernels.
+// Register/LDS layout of one transform inside the blind-rotation kernels.
 //
-// A ciphertext's polynomial of N = 2^LOGN coefficients is spread over
-// T = N / E threads holding E = 2^LOGE values each.  The negacyclic NTT
-// (Cooley-Tukey forward, Gentleman-Sande inverse, twiddles in bit-reversed
-// order) is split into passes; pass p owns a window of LOGE index bits
-// starting at bit w(p), and thread t's element e is coefficient
+// The ring product works on the folded polynomial of n = N/2 complex points
+// (coefficients j and j + n of a real polynomial form point j).  A transform
+// of 2^LOGN points is spread over T = 2^LOGN / E threads holding E = 2^LOGE
+// points each.  The transform (Cooley-Tukey forward, Gentleman-Sande inverse,
+// one twiddle per butterfly block) is split into passes; pass p owns a window
+// of LOGE index bits starting at bit w(p), and thread t's element e is point
 //
 //     j = (t mod 2^w) | (e << w) | ((t >> w) << (w + LOGE)),
 //
 // so every butterfly of the stages whose bit lies in the window is in
-// registers.  Between passes the polynomial is transposed through LDS.
+// registers.  Between passes the points are transposed through LDS.
 // Pass 0 (window at the top) is the coefficient layout j = t + T*e used for
 // rotation, decomposition and the accumulator; the last pass (window at bit 0)
 // is the transform-domain layout, in which the bootstrapping key is stored.
@@ -25,16 +26,14 @@
 
 namespace gt {
 
-// log2 of the values per thread for a ring of degree 2^logn (host and device)
-constexpr GL_HD int log_values_per_thread(int logn) { return logn >= 9 ? 3 : logn - 6; }
+// complex points per thread of the ring transform (log2)
+constexpr int kRingLogE = 2;
 
-template <int LOGN_>
+template <int LOGN_, int LOGE_>
 struct Layout {
   static constexpr int LOGN = LOGN_;
   static constexpr int N = 1 << LOGN;
-  // 8 values per thread (4 at N = 256): the four transform-domain
-  // accumulators of an external product then take 64 registers per thread
-  static constexpr int LOGE = log_values_per_thread(LOGN);
+  static constexpr int LOGE = LOGE_;
   static constexpr int E = 1 << LOGE;
   static constexpr int LOGT = LOGN - LOGE;
   static constexpr int T = 1 << LOGT;
@@ -48,8 +47,12 @@ struct Layout {
   static GL_HD int jmap(int t, int e, int w) {
     return (t & ((1 << w) - 1)) | (e << w) | ((t >> w) << (w + LOGE));
   }
-  // coefficient index of (t, e) in the transform-domain layout
+  // point index of (t, e) in the transform-domain layout
   static GL_HD int jfinal(int t, int e) { return jmap(t, e, win(NPASS - 1)); }
 };
+
+// the ring transform for ring degree 2^LOGN_RING: 2^(LOGN_RING-1) complex points
+template <int LOGN_RING>
+using RingLayout = Layout<LOGN_RING - 1, kRingLogE>;
 
 }  // namespace gt

@@ -68,6 +68,7 @@ _SIGNATURES = {
     "glyph_relu_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
+    "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
     "tfhe_stage_timing": (ctypes.c_int, [ctypes.c_int]),
     "tfhe_stage_times": (ctypes.c_int, [_vp, _vp]),
 }
@@ -175,6 +176,15 @@ def tfhe_keygen_from_seed(params, seed: int, device: int = 0):
     hs, he = ctypes.c_void_p(), ctypes.c_void_p()
     _check(lib().tfhe_keygen_from_seed(ctypes.byref(p), seed, device, ctypes.byref(hs), ctypes.byref(he)))
     return SecretKey(hs, p), EvalKey(he, p, device)
+
+
+def tfhe_transform_error_bound(params):
+    """(key_parts, worst-case transform error) for a parameter set."""
+    p = make_params(params)
+    parts = ctypes.c_int32()
+    bound = ctypes.c_double()
+    _check(lib().tfhe_transform_error_bound(ctypes.byref(p), ctypes.byref(parts), ctypes.byref(bound)))
+    return parts.value, bound.value
 
 
 def tfhe_export_keys(sk: SecretKey) -> dict:

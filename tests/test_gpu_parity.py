@@ -75,8 +75,8 @@ PRODUCT_PARAMS = {
 
 @pytest.mark.parametrize("N", [256, 512, 1024, 2048])
 def test_negacyclic_product_exact(torch, N):
-    """The fp64 NTT product equals the schoolbook product mod 2^32, including
-    inputs at the extremes of the exactness bound."""
+    """The fp64 transform product, rounded, equals the schoolbook product mod
+    2^32, including inputs at the extremes of the error bound."""
     p = PRODUCT_PARAMS[N]
     _, ek, _ = keys_for(f"product{N}", torch, p, 7)
     half = 1 << (p["bg_bit"] - 1)
@@ -84,14 +84,22 @@ def test_negacyclic_product_exact(torch, N):
     B = 7  # more than one block of polynomials and a ragged tail
     d = rng.integers(-half, half, (B, N)).astype(np.int32)
     b = rng.integers(0, M32, (B, N), dtype=np.uint64).astype(np.uint32)
-    # extremes: all digits -Bg/2 against coefficients whose 16-bit halves are
-    # both at their largest magnitude (hi = -2^15, lo = -2^15), and mixed signs
+    # extremes: all digits -Bg/2 against coefficients whose signed key parts
+    # (16-bit halves at N <= 1024, 11-bit thirds at N = 2048) are all at their
+    # largest magnitude with one sign, and alternating digit signs
+    if N <= 1024:
+        ext_neg, ext_pos = -(1 << 31), (1 << 31) - (1 << 15)          # halves (-2^15, 0), (2^15, -2^15)
+    else:
+        ext_neg = -1024 - 1024 * 2**11 - 511 * 2**22                   # thirds (-1024, -1024, -511)
+        ext_pos = 1023 + 1023 * 2**11 + 511 * 2**22                    # thirds (1023, 1023, 511)
     d[0] = -half
-    b[0] = np.uint32(0x7FFF8000)  # signed value 2^31 - 2^15: hi = 2^15, lo = -2^15
+    b[0] = np.uint32(ext_neg % M32)
     d[1] = -half
-    b[1] = np.uint32(0x80008000)  # -2^31 + 2^15 - 2^16... extreme negative halves
+    b[1] = np.uint32(ext_pos % M32)
     d[2] = np.where(np.arange(N) % 2 == 0, -half, half - 1)
-    b[2] = np.uint32(0x80000000)
+    b[2] = np.where(np.arange(N) % 2 == 0, ext_neg % M32, ext_pos % M32).astype(np.uint32)
+    d[3] = half - 1
+    b[3] = np.uint32(ext_neg % M32)
     say(f"negacyclic product N={N} B={B}")
     out = tfhe.to_host(tfhe.tfhe_negacyclic_mul_batch(ek, torch.from_numpy(d).cuda(), tfhe.to_device(b)))
     torch.cuda.synchronize()
