@@ -269,8 +269,9 @@ struct BkCtx {
 void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
   const BkCtx& c = *static_cast<BkCtx*>(vctx);
   const int N = c.p->N, n = N / 2;
-  const int E = 1 << kRingLogE, T = n >> kRingLogE;
   const int S = c.parts;
+  const int loge = ring_log_e(S);
+  const int E = 1 << loge, T = n >> loge;
   std::vector<std::vector<ComplexL>> z(S, std::vector<ComplexL>(n));
   int64_t piece_lo[4], piece_hi[4];
   for (int64_t row = begin; row < end; row++) {  // row = (i * 2l + r) * 2 + q
@@ -288,7 +289,7 @@ void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
       double* dst = c.out + ((ir * 2 * S + q * S + s) * static_cast<int64_t>(n)) * 2;
       for (int t = 0; t < T; t++)
         for (int e = 0; e < E; e++) {
-          const int j = e | (t << kRingLogE);  // point held by (t, e) after the forward transform
+          const int j = e | (t << loge);  // point held by (t, e) after the forward transform
           const int slot = e * T + t;
           dst[2 * slot] = static_cast<double>(z[s][j].re / static_cast<long double>(n));
           dst[2 * slot + 1] = static_cast<double>(z[s][j].im / static_cast<long double>(n));

@@ -75,25 +75,20 @@ __device__ __forceinline__ uint32_t round_low32(double v) {
 }
 
 // Make LDS writes of all threads of a polynomial visible to its other threads.
-// A polynomial held by one wave needs only ordering (a wave's LDS operations
-// complete in order); a polynomial spread over several waves needs the block
-// barrier.
+// A polynomial held by one wave needs only ordering: a wave's LDS operations
+// are performed in issue order, so a wavefront-scope fence emits no wait and
+// only keeps the compiler from moving LDS accesses across it.  A polynomial
+// spread over several waves needs the block barrier.
 template <int T>
 __device__ __forceinline__ void poly_sync() {
   if constexpr (T <= 64) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   } else {
     __syncthreads();
   }
 }
-
-// bank swizzle of the transpose scratch: with 4 complex (16-byte) points per
-// thread every pass layout at n = 128..1024 reads and writes without bank
-// conflicts (checked for 32 and 64 banks of 4 bytes); it permutes only the
-// low 4 bits, so it stays inside the polynomial
-__device__ __forceinline__ int swz(int j) { return j ^ (((j >> 1) ^ (j >> 2)) & 15); }
 
 // Position of twiddle k in the LDS copy of the twiddle table.  Stage s owns
 // k in [n/2^(s+1), n/2^s); in a pass other than the first, thread t reads the
@@ -120,14 +115,23 @@ __host__ __device__ constexpr int tw_lds_slot(int k) {
 
 template <class Lay, int WFROM, int WTO>
 __device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* scr) {
+  // one base address per layout where the slots are affine in e (immediate offsets)
+  double2* wr = scr + Lay::slot(Lay::jmap(t, 0, WFROM));
+  double2* rd = scr + Lay::slot(Lay::jmap(t, 0, WTO));
   static_for<0, Lay::E>([&](auto EI) {
     constexpr int e = decltype(EI)::value;
-    scr[swz(Lay::jmap(t, e, WFROM))] = x[e];
+    if constexpr (Lay::affine(WFROM))
+      wr[e * Lay::slot_stride(WFROM)] = x[e];
+    else
+      scr[Lay::slot(Lay::jmap(t, e, WFROM))] = x[e];
   });
   poly_sync<Lay::T>();
   static_for<0, Lay::E>([&](auto EI) {
     constexpr int e = decltype(EI)::value;
-    x[e] = scr[swz(Lay::jmap(t, e, WTO))];
+    if constexpr (Lay::affine(WTO))
+      x[e] = rd[e * Lay::slot_stride(WTO)];
+    else
+      x[e] = scr[Lay::slot(Lay::jmap(t, e, WTO))];
   });
   poly_sync<Lay::T>();
 }
@@ -318,13 +322,13 @@ __global__ __launch_bounds__(256) void prep_kernel(int mode, int gate, const uin
 // Ring degree 2^LOGN, key coefficients split into S signed parts.
 template <int LOGN, int S>
 struct BrCfg {
-  using Lay = RingLayout<LOGN>;
+  using Lay = RingLayout<LOGN, S>;
   static constexpr int NR = 1 << LOGN;  // ring degree
   static constexpr int NC = Lay::N;     // complex points, NR / 2
   static constexpr int E = Lay::E, T = Lay::T;
   static constexpr int O = 2 * S;       // transform-domain accumulators: (mask, body) x parts
   static constexpr int SHIFT = S == 2 ? 16 : 11;
-  // ciphertexts per block (two at T = 128: measured faster than one or four)
+  // ciphertexts per block: 256 threads (one wave per ciphertext at N = 1024)
 #ifdef GT_BR_CPB
   static constexpr int CPB = GT_BR_CPB;
 #else
@@ -332,6 +336,17 @@ struct BrCfg {
 #endif
   static constexpr int THREADS = CPB * T;
 };
+
+// 16-byte load through a buffer resource (base and size uniform, offset per
+// lane): no per-lane 64-bit address arithmetic, and an offset past the size
+// returns zero instead of faulting
+__device__ __forceinline__ double2 load_b128(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+  double2 d;
+  __builtin_memcpy(&d, &v, sizeof d);
+  return d;
+}
 
 template <int LOGN, int S>
 __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
@@ -342,7 +357,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
   using Lay = typename C::Lay;
   constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
   __shared__ double2 s_tw[NC];
-  __shared__ double2 s_scr[CPB * NC];
+  __shared__ double2 s_scr[CPB * Lay::SCR];
   __shared__ uint32_t s_acc[CPB * 2 * NR];
 
   const int slot = threadIdx.x / T;
@@ -353,7 +368,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
 
   for (int k = threadIdx.x; k < NC; k += C::THREADS) s_tw[tw_lds_slot<Lay>(k)] = tw_g[k];
   __syncthreads();
-  double2* scr = s_scr + slot * NC;
+  double2* scr = s_scr + slot * Lay::SCR;
   uint32_t* acc_a = s_acc + slot * 2 * NR;
   uint32_t* acc_b = acc_a + NR;
   const uint16_t* ab = abar + c * (n + 1);
@@ -386,11 +401,15 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
   uint32_t offset = 0;
   for (int j = 1; j <= l; j++) offset += half << (32 - j * bg_bit);
   if (l * bg_bit < 32) offset += 1u << (31 - l * bg_bit);
-  const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;
+  const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;  // points per CMux
+  // key of one CMux: [2l][O][E][T] points; lane t reads point (r, o, e, t)
+  const uint32_t voff = static_cast<uint32_t>(t) * 16u;
 
   for (int i = 0; i < n; i++) {
     const uint32_t a_i = ab[i];
-    const double2* bki = bk + static_cast<size_t>(i) * bk_step;
+    const __amdgpu_buffer_rsrc_t bkr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
+                                          static_cast<int>(bk_step * 16), 0x00020000);
     double2 acc[O][E];
 #pragma unroll
     for (int o = 0; o < O; o++)
@@ -399,6 +418,10 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
 
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
+      // recompute the rotation indices for each q instead of keeping 2E of
+      // them live across the transforms (the empty asm hides a_i's value)
+      uint32_t a_q = a_i;
+      asm volatile("" : "+v"(a_q));
       // D = X^{a_i} P - P (plus the decomposition offset) at coefficients
       // t + T*e (h = 0) and t + T*e + NR/2 (h = 1): point e's real and imaginary part
       uint32_t D[2][E];
@@ -407,7 +430,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
 #pragma unroll
         for (int h = 0; h < 2; h++) {
           const int j = t + T * e + h * NC;
-          D[h][e] = rot_coef<NR>(P, a_i, j) - P[j] + offset;
+          D[h][e] = rot_coef<NR>(P, a_q, j) - P[j] + offset;
         }
       for (int jj = 0; jj < l; jj++) {
         const int shift = 32 - (jj + 1) * bg_bit;
@@ -418,24 +441,15 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
               static_cast<double>(static_cast<int32_t>((D[0][e] >> shift) & dmask) - static_cast<int32_t>(half)),
               static_cast<double>(static_cast<int32_t>((D[1][e] >> shift) & dmask) - static_cast<int32_t>(half)));
         fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
-        // key row r = q*l + jj: O outputs [o][e][t], one 16-byte point per load
-        const double2* bkr = bki + static_cast<size_t>(q * l + jj) * O * NC + t;
-        double2 w[E];
-#pragma unroll
-        for (int e = 0; e < E; e++) w[e] = bkr[e * T];
+        // key row r = q*l + jj
+        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
 #pragma unroll
         for (int o = 0; o < O; o++) {
-          double2 wn[E];
-          if (o + 1 < O) {
+          double2 w[E];
 #pragma unroll
-            for (int e = 0; e < E; e++) wn[e] = bkr[((o + 1) * E + e) * T];
-          }
+          for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>((o * E + e) * T * 16));
 #pragma unroll
           for (int e = 0; e < E; e++) cmac(acc[o][e], x[e], w[e]);
-          if (o + 1 < O) {
-#pragma unroll
-            for (int e = 0; e < E; e++) w[e] = wn[e];
-          }
         }
       }
     }
@@ -722,16 +736,16 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double2* __re
                                                              const int32_t* __restrict__ d,
                                                              const uint32_t* __restrict__ b,
                                                              uint32_t* __restrict__ c, int64_t B) {
-  using Lay = RingLayout<LOGN>;
+  using Lay = RingLayout<LOGN, S>;
   constexpr int NR = 1 << LOGN, NC = Lay::N, E = Lay::E, T = Lay::T, CPB = 256 / T;
   constexpr int SHIFT = S == 2 ? 16 : 11;
-  __shared__ double2 s_scr[CPB * NC];
+  __shared__ double2 s_scr[CPB * Lay::SCR];
   const int slot = threadIdx.x / T;
   const int t = threadIdx.x % T;
   int64_t k = static_cast<int64_t>(blockIdx.x) * CPB + slot;
   const bool active = k < B;
   if (!active) k = B - 1;
-  double2* scr = s_scr + slot * NC;
+  double2* scr = s_scr + slot * Lay::SCR;
   double2 xd[E], xb[S][E];
 #pragma unroll
   for (int e = 0; e < E; e++) {
@@ -798,7 +812,7 @@ int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* test
 template <int LOGN, int S>
 int launch_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c, int64_t B,
                hipStream_t st) {
-  constexpr int CPB = 256 / RingLayout<LOGN>::T;
+  constexpr int CPB = 256 / RingLayout<LOGN, S>::T;
   const int64_t blocks = (B + CPB - 1) / CPB;
   hipLaunchKernelGGL((negacyclic_mul_kernel<LOGN, S>), dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st,
                      reinterpret_cast<const double2*>(ek->tw), d, b, c, B);

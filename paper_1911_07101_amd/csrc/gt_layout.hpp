@@ -26,8 +26,10 @@
 
 namespace gt {
 
-// complex points per thread of the ring transform (log2)
-constexpr int kRingLogE = 2;
+// log2 of the complex points per thread of the ring transform: 8 points when
+// the key is split into two parts (a lane's four transform-domain accumulators
+// then take 128 registers), 4 points with three parts (six accumulators)
+GL_HD constexpr int ring_log_e(int parts) { return parts == 2 ? 3 : 2; }
 
 template <int LOGN_, int LOGE_>
 struct Layout {
@@ -49,10 +51,28 @@ struct Layout {
   }
   // point index of (t, e) in the transform-domain layout
   static GL_HD int jfinal(int t, int e) { return jmap(t, e, win(NPASS - 1)); }
+
+  // LDS slot of point j in the transpose scratch.  8 points per thread: one
+  // pad slot after every 8 points; the slot of jmap(t, e, w) is then an
+  // affine function of e (for w = 0 or w >= 3) and every group of 8
+  // consecutive lanes touches 8 distinct 16-byte bank groups in each pass
+  // layout.  4 points per thread: the low 4 bits are XORed with bits 1..4,
+  // which is conflict-free for every pass layout of 128..1024 points.
+  static GL_HD int slot(int j) {
+    if constexpr (LOGE == 3)
+      return j + (j >> 3);
+    else
+      return j ^ (((j >> 1) ^ (j >> 2)) & 15);
+  }
+  static constexpr int SCR = LOGE == 3 ? N + N / 8 : N;  // scratch slots per polynomial
+  // slot(jmap(t, e, w)) = slot(jmap(t, 0, w)) + e * slot_stride(w) when affine(w)
+  static constexpr GL_HD bool affine(int w) { return LOGE == 3 && (w == 0 || w >= 3); }
+  static constexpr GL_HD int slot_stride(int w) { return w == 0 ? 1 : (1 << w) + (1 << (w - 3)); }
 };
 
-// the ring transform for ring degree 2^LOGN_RING: 2^(LOGN_RING-1) complex points
-template <int LOGN_RING>
-using RingLayout = Layout<LOGN_RING - 1, kRingLogE>;
+// the ring transform for ring degree 2^LOGN_RING (2^(LOGN_RING-1) complex
+// points) with the key split into S parts
+template <int LOGN_RING, int S>
+using RingLayout = Layout<LOGN_RING - 1, ring_log_e(S)>;
 
 }  // namespace gt
