@@ -36,11 +36,7 @@ namespace {
 
 constexpr uint32_t kMu = 0x20000000u;  // 1/8
 
-// minimum waves per SIMD the blind-rotation kernel is compiled for (sets its
-// register budget: 2 -> 256 VGPRs, 3 -> 168)
-#ifndef GT_BR_WAVES_PER_SIMD
-#define GT_BR_WAVES_PER_SIMD 2
-#endif
+
 
 template <int B, int E, class F>
 __device__ __forceinline__ void static_for(F&& f) {
@@ -136,64 +132,56 @@ __device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* 
   poly_sync<Lay::T>();
 }
 
-// Offset of stage k's twiddles within a pass's batch: the stages before it
-// (descending bits for the forward transform, ascending for the inverse) use
-// E >> (b + 1) twiddles each, b the stage's bit within the pass window.
-template <class Lay>
-constexpr int tw_offset(int p, int k, bool fwd) {
-  int off = 0;
-  for (int q = 0; q < k; q++) {
-    const int s = fwd ? Lay::hi(p) - 1 - q : Lay::lo(p) + q;
-    off += Lay::E >> (s - Lay::win(p) + 1);
-  }
-  return off;
+// Twiddle g of stage s (bit b of the window at w) for thread t: pass 0's are
+// the same for every thread (tw_uniform, global memory, read through the
+// scalar cache), the others come from tw, an LDS copy laid out by
+// tw_lds_slot (TW_PERMUTED) or a natural-order table.
+template <class Lay, bool TW_PERMUTED, int p, int s, int g>
+__device__ __forceinline__ double2 twiddle(int t, const double2* __restrict__ tw,
+                                           const double2* __restrict__ tw_uniform) {
+  constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
+  constexpr int w = Lay::win(p);
+  constexpr int b = s - w;
+  constexpr int G = E >> (b + 1);
+  if constexpr (p == 0)
+    return tw_uniform[(N >> (s + 1)) + g];
+  else if constexpr (TW_PERMUTED)
+    return tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
+  else
+    return tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
 }
 
 // Forward transform of the folded polynomial over C[X]/(X^n - i)
 // (Cooley-Tukey butterflies; the block of point j at stage s splits tree node
 // k = n/2^(s+1) + j/2^(s+1) and multiplies by tw[k]).  In: pass-0 (coefficient)
-// layout; out: last-pass (transform) layout.  The twiddles of a pass are
-// fetched together before its butterflies: pass 0's are the same for every
-// thread (tw_uniform, global memory), the others come from tw, an LDS copy
-// laid out by tw_lds_slot (TW_PERMUTED) or a natural-order table.
+// layout; out: last-pass (transform) layout.  Each stage fetches its own
+// twiddles (one per butterfly group of the thread).
 template <class Lay, bool TW_PERMUTED>
 __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2* scr,
                                             const double2* __restrict__ tw,
                                             const double2* __restrict__ tw_uniform) {
-  constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
+  constexpr int E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
     if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w>(x, t, scr);
-    double2 z[E];
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
       constexpr int b = s - w;
       constexpr int G = E >> (b + 1);
-      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, true);
+      double2 z[G];
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
-        if constexpr (p == 0)
-          z[off + g] = tw_uniform[(N >> (s + 1)) + g];
-        else if constexpr (TW_PERMUTED)
-          z[off + g] = tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
-        else
-          z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
+        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform);
       });
-    });
-    static_for<0, NS>([&](auto SI) {
-      constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
-      constexpr int b = s - w;
-      constexpr int G = E >> (b + 1);
-      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, true);
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
           const double2 u = x[e];
-          const double2 v = cmul(x[e2], z[off + g]);
+          const double2 v = cmul(x[e2], z[g]);
           x[e] = cadd(u, v);
           x[e2] = csub(u, v);
         });
@@ -202,48 +190,43 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
   });
 }
 
-// Inverse transform without the 1/n factor (Gentleman-Sande butterflies with
-// the conjugate twiddles).  In: transform layout; out: coefficient layout.
-template <class Lay, bool TW_PERMUTED>
-__device__ __forceinline__ void fft_inverse(double2 (&x)[Lay::E], int t, double2* scr,
+// Inverse transforms without the 1/n factor (Gentleman-Sande butterflies with
+// the conjugate twiddles) of polynomials x[K0 .. K0+K) at once: they share
+// each stage's twiddles, and one polynomial's transpose is in flight while
+// another's butterflies run.  In: transform layout; out: coefficient layout.
+template <class Lay, bool TW_PERMUTED, int K0, int K, int M>
+__device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, double2* scr,
                                             const double2* __restrict__ tw,
                                             const double2* __restrict__ tw_uniform) {
-  constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
+  static_assert(K0 + K <= M, "polynomial range");
+  constexpr int E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = Lay::NPASS - 1 - decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
-    if constexpr (p < Lay::NPASS - 1) transpose<Lay, Lay::win(p + 1), w>(x, t, scr);
-    double2 z[E];
+    if constexpr (p < Lay::NPASS - 1)
+      static_for<K0, K0 + K>([&](auto KI) { transpose<Lay, Lay::win(p + 1), w>(x[decltype(KI)::value], t, scr); });
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::lo(p) + decltype(SI)::value;
       constexpr int b = s - w;
       constexpr int G = E >> (b + 1);
-      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, false);
+      double2 z[G];
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
-        if constexpr (p == 0)
-          z[off + g] = tw_uniform[(N >> (s + 1)) + g];
-        else if constexpr (TW_PERMUTED)
-          z[off + g] = tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
-        else
-          z[off + g] = tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
+        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform);
       });
-    });
-    static_for<0, NS>([&](auto SI) {
-      constexpr int s = Lay::lo(p) + decltype(SI)::value;
-      constexpr int b = s - w;
-      constexpr int G = E >> (b + 1);
-      constexpr int off = tw_offset<Lay>(p, decltype(SI)::value, false);
-      static_for<0, G>([&](auto GI) {
-        constexpr int g = decltype(GI)::value;
-        static_for<0, (1 << b)>([&](auto LI) {
-          constexpr int e = (g << (b + 1)) | decltype(LI)::value;
-          constexpr int e2 = e | (1 << b);
-          const double2 u = x[e];
-          const double2 v = x[e2];
-          x[e] = cadd(u, v);
-          x[e2] = cmul_conj(csub(u, v), z[off + g]);
+      static_for<K0, K0 + K>([&](auto KI) {
+        constexpr int k = decltype(KI)::value;
+        static_for<0, G>([&](auto GI) {
+          constexpr int g = decltype(GI)::value;
+          static_for<0, (1 << b)>([&](auto LI) {
+            constexpr int e = (g << (b + 1)) | decltype(LI)::value;
+            constexpr int e2 = e | (1 << b);
+            const double2 u = x[k][e];
+            const double2 v = x[k][e2];
+            x[k][e] = cadd(u, v);
+            x[k][e2] = cmul_conj(csub(u, v), z[g]);
+          });
         });
       });
     });
@@ -329,12 +312,13 @@ struct BrCfg {
   static constexpr int O = 2 * S;       // transform-domain accumulators: (mask, body) x parts
   static constexpr int SHIFT = S == 2 ? 16 : 11;
   // ciphertexts per block: 256 threads (one wave per ciphertext at N = 1024)
-#ifdef GT_BR_CPB
-  static constexpr int CPB = GT_BR_CPB;
-#else
   static constexpr int CPB = T >= 256 ? 1 : 256 / T;
-#endif
   static constexpr int THREADS = CPB * T;
+  static constexpr int SCR = Lay::SCR;
+  static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4;
+  // two blocks (two waves per SIMD, 256 registers each) when their LDS fits
+  // in the CU's 160 KB, else one
+  static constexpr int MIN_WAVES = 2 * LDS_BYTES <= 160 * 1024 ? 2 : 1;
 };
 
 // 16-byte load through a buffer resource (base and size uniform, offset per
@@ -349,7 +333,7 @@ __device__ __forceinline__ double2 load_b128(__amdgpu_buffer_rsrc_t r, uint32_t 
 }
 
 template <int LOGN, int S>
-__global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) void blind_rotate_kernel(
+__global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAVES)) void blind_rotate_kernel(
     const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
     int64_t B) {
@@ -396,16 +380,25 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
     poly_sync<T>();
   }
 
+  // signed gadget decomposition: adding the offset (Bg/2 in every digit
+  // position, plus the rounding bit below the last digit) turns each signed
+  // digit d into the unsigned field d + Bg/2; flipping the field's top bit
+  // (flip) then makes the field's sign extension equal to d
   const uint32_t half = 1u << (bg_bit - 1);
-  const uint32_t dmask = (1u << bg_bit) - 1u;
-  uint32_t offset = 0;
-  for (int j = 1; j <= l; j++) offset += half << (32 - j * bg_bit);
+  uint32_t offset = 0, flip = 0;
+  for (int j = 1; j <= l; j++) {
+    offset += half << (32 - j * bg_bit);
+    flip |= half << (32 - j * bg_bit);
+  }
   if (l * bg_bit < 32) offset += 1u << (31 - l * bg_bit);
   const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;  // points per CMux
   // key of one CMux: [2l][O][E][T] points; lane t reads point (r, o, e, t)
   const uint32_t voff = static_cast<uint32_t>(t) * 16u;
 
   for (int i = 0; i < n; i++) {
+    // keep the block's ciphertexts on the same CMux: they then read the same
+    // key points close together in time, which the L1 cache serves
+    if constexpr (CPB > 1 && T <= 64) __syncthreads();
     const uint32_t a_i = ab[i];
     const __amdgpu_buffer_rsrc_t bkr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
@@ -430,32 +423,40 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), GT_BR_WAVES_PER_SIMD) vo
 #pragma unroll
         for (int h = 0; h < 2; h++) {
           const int j = t + T * e + h * NC;
-          D[h][e] = rot_coef<NR>(P, a_q, j) - P[j] + offset;
+          D[h][e] = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
         }
       for (int jj = 0; jj < l; jj++) {
-        const int shift = 32 - (jj + 1) * bg_bit;
+        // digit jj sits in bits [32 - (jj+1) bg_bit, 32 - jj bg_bit): move it
+        // to the top, then shift it down arithmetically (sign extension)
+        const uint32_t lsh = static_cast<uint32_t>(jj * bg_bit), rsh = static_cast<uint32_t>(32 - bg_bit);
+        // key row r = q*l + jj; its first output's points are requested
+        // before the transform so that their latency overlaps it
+        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
+        double2 w[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>(e * T * 16));
         double2 x[E];
 #pragma unroll
         for (int e = 0; e < E; e++)
-          x[e] = make_double2(
-              static_cast<double>(static_cast<int32_t>((D[0][e] >> shift) & dmask) - static_cast<int32_t>(half)),
-              static_cast<double>(static_cast<int32_t>((D[1][e] >> shift) & dmask) - static_cast<int32_t>(half)));
+          x[e] = make_double2(static_cast<double>(static_cast<int32_t>(D[0][e] << lsh) >> rsh),
+                              static_cast<double>(static_cast<int32_t>(D[1][e] << lsh) >> rsh));
         fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
-        // key row r = q*l + jj
-        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
 #pragma unroll
         for (int o = 0; o < O; o++) {
-          double2 w[E];
+          if (o > 0) {
 #pragma unroll
-          for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>((o * E + e) * T * 16));
+            for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>((o * E + e) * T * 16));
+          }
 #pragma unroll
           for (int e = 0; e < E; e++) cmac(acc[o][e], x[e], w[e]);
         }
       }
     }
 
-#pragma unroll
-    for (int o = 0; o < O; o++) fft_inverse<Lay, true>(acc[o], t, scr, s_tw, tw_g);
+    // inverse transforms two at a time (O is even)
+    static_for<0, O / 2>([&](auto PI) {
+      fft_inverse<Lay, true, 2 * decltype(PI)::value, 2>(acc, t, scr, s_tw, tw_g);
+    });
     // every output is within 1/8 of an integer (the transform's error bound):
     // round, take it mod 2^32 and recombine the key parts
 #pragma unroll
@@ -620,10 +621,7 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
 // rows are fetched one coefficient ahead.  Every table read, add and the
 // final subtraction are exact mod 2^32.
 constexpr int KS8_WAVES = 4;
-#ifndef GT_KS8_CB
-#define GT_KS8_CB 16
-#endif
-constexpr int KS8_CB = GT_KS8_CB;  // samples per wave
+constexpr int KS8_CB = 16;  // samples per wave
 
 __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __restrict__ in,
                                                              const uint32_t* __restrict__ ksk,
@@ -767,16 +765,16 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double2* __re
     }
   }
   fft_forward<Lay, false>(xd, t, scr, tw, tw);
-#pragma unroll
-  for (int sp = 0; sp < S; sp++) {
+  static_for<0, S>([&](auto SP) {
+    constexpr int sp = decltype(SP)::value;
     fft_forward<Lay, false>(xb[sp], t, scr, tw, tw);
 #pragma unroll
     for (int e = 0; e < E; e++) {
       const double2 pr = cmul(xd[e], xb[sp][e]);
       xb[sp][e] = make_double2(pr.x / NC, pr.y / NC);  // exact: NC is a power of two
     }
-    fft_inverse<Lay, false>(xb[sp], t, scr, tw, tw);
-  }
+    fft_inverse<Lay, false, sp, 1>(xb, t, scr, tw, tw);
+  });
   if (!active) return;
 #pragma unroll
   for (int e = 0; e < E; e++) {
