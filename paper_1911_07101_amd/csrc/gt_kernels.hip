@@ -612,103 +612,107 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
   }
 }
 
-// Key switching for t = 8 digits of 2 bits (16-bit precision).  A block of 4
-// waves covers 64 output columns of 4 x 32 samples.  For each input
-// coefficient i the block builds, in LDS, the pair tables
+// Key switching for t = 8 digits of 2 bits (16-bit precision), one sample per
+// thread.  A block of 256 threads covers 256 samples and KS8_COLS output
+// columns.  For each input coefficient i the block builds, in LDS, the pair
+// tables
 //   PT[p][u][col] = KSK[i][2p][u >> 2] + KSK[i][2p+1][u & 3]   (row of value 0 = 0)
-// for the 4 digit pairs p and the 16 pair values u; a sample then needs 4
-// table reads for the 8 digits.  Tables are double-buffered across i; the key
-// rows are fetched one coefficient ahead.  Every table read, add and the
-// final subtraction are exact mod 2^32.
-constexpr int KS8_WAVES = 4;
-constexpr int KS8_CB = 16;  // samples per wave
+// for the 4 digit pairs p and the 16 pair values u; a thread then reads, for
+// each of its 4 pair values, the table row of that value with 16-byte loads
+// (4 columns each) and subtracts the 4 rows from its KS8_COLS outputs.  The
+// digits are taken once per sample and input coefficient, the row addresses
+// once per pair, and the column offsets are immediates.  Tables are
+// double-buffered across i (one barrier per i); the key rows are fetched
+// ahead.  Every table read, add and the final subtraction are exact
+// mod 2^32.
+constexpr int KS8_COLS = 16;               // output columns per block
+constexpr int KS8_RS = KS8_COLS + 4;       // padded table row stride (words)
+constexpr int KS8_TAB = 64;                // 4 pairs x 16 pair values
 
 __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __restrict__ in,
                                                              const uint32_t* __restrict__ ksk,
                                                              uint32_t* __restrict__ out, int n, int N,
                                                              int64_t B, int mode, int32_t bits,
                                                              int64_t gate_begin) {
-  constexpr int ROWS = 24;              // 8 digits x 3 non-zero values
-  constexpr int TAB = 64;               // 4 pairs x 16 pair values
-  __shared__ uint32_t s_tab[2][TAB][KS_COLS];
-  __shared__ uint32_t s_in[KS8_WAVES * KS8_CB][KS_ICH];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int col = blockIdx.y * KS_COLS + lane;
-  const bool col_ok = col <= n;
-  const int64_t c0 = static_cast<int64_t>(blockIdx.x) * (KS8_WAVES * KS8_CB);
-  const int64_t cw = c0 + wave * KS8_CB;
+  constexpr int ROWS = 24;  // 8 digits x 3 non-zero values
+  __shared__ __align__(16) uint32_t s_tab[2][KS8_TAB * KS8_RS];
+  const int tid = threadIdx.x;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + tid;
+  const bool c_ok = c < B;
+  const int col0 = blockIdx.y * KS8_COLS;
   const size_t row = static_cast<size_t>(n) + 1;
+  const uint32_t* x_in = in + (c_ok ? c : B - 1) * (N + 1);
 
-  uint32_t acc[KS8_CB];
+  uint32_t acc[KS8_COLS];
 #pragma unroll
-  for (int k = 0; k < KS8_CB; k++) {
-    const int64_t c = cw + k;
-    acc[k] = (col == n && c < B) ? in[c * (N + 1) + N] : 0u;
-  }
+  for (int j = 0; j < KS8_COLS; j++) acc[j] = col0 + j == n ? x_in[N] : 0u;
 
-  // thread (wave, lane) fetches key rows wave*6 .. wave*6+5 of its column and
-  // builds table entries (pair = wave, all 16 values) -- the two digit rows a
-  // pair needs are rows 6*wave .. 6*wave+5, exactly this thread's fetch
-  uint32_t kr[6];
-  auto fetch = [&](int i) {
-    const uint32_t* base = ksk + static_cast<size_t>(i) * ROWS * row + col;
+  // table building: thread (p, col, half) = (tid >> 6 & 3, tid & 15, tid >> 4 & 3)
+  // fetches key rows of pair p at column col0 + col and writes the 4 entries
+  // u = 4 * half + v2: PT[p][u] = row(2p, half) + row(2p+1, v2), row(., 0) = 0
+  const int b_col = tid & 15, b_half = (tid >> 4) & 3, b_pair = tid >> 6;
+  const bool b_ok = col0 + b_col <= n;
+  // key rows of coefficient i + d in kr[d] (element 0: row(2p, half),
+  // elements 1..3: row(2p+1, 1..3)) and inputs x_i+d in xq[d]: both are
+  // fetched ahead (key rows three coefficients, inputs four), so their
+  // latency is covered by the table lookups in between
+  uint32_t kr[3][4];
+  auto fetch = [&](int i, uint32_t (&k)[4]) {
+    const uint32_t* base = ksk + static_cast<size_t>(i) * ROWS * row + col0 + b_col;
+    k[0] = (b_ok && b_half) ? base[static_cast<size_t>(b_pair * 6 + b_half - 1) * row] : 0u;
 #pragma unroll
-    for (int q = 0; q < 6; q++) kr[q] = col_ok ? base[static_cast<size_t>(wave * 6 + q) * row] : 0u;
+    for (int v = 1; v <= 3; v++) k[v] = b_ok ? base[static_cast<size_t>(b_pair * 6 + 2 + v) * row] : 0u;
   };
-  auto build = [&](int b) {
-    // kr[0..2]: digit 2*wave, values 1..3; kr[3..5]: digit 2*wave+1, values 1..3
+  for (int d = 0; d < 3; d++) fetch(min(d, N - 1), kr[d]);
+  uint32_t xq[4];
 #pragma unroll
-    for (int u = 0; u < 16; u++) {
-      const int v1 = u >> 2, v2 = u & 3;
-      const uint32_t a = v1 ? kr[v1 - 1] : 0u;
-      const uint32_t c = v2 ? kr[2 + v2] : 0u;
-      s_tab[b][wave * 16 + u][lane] = a + c;
+  for (int d = 0; d < 4; d++) xq[d] = x_in[min(d, N - 1)];
+
+#pragma unroll 1
+  for (int i = 0; i < N; i++) {
+    const int b = i & 1;
+    {
+      uint32_t* tab = s_tab[b] + (b_pair * 16 + b_half * 4) * KS8_RS + b_col;
+#pragma unroll
+      for (int v2 = 0; v2 < 4; v2++) tab[v2 * KS8_RS] = kr[0][0] + (v2 ? kr[0][v2] : 0u);
     }
-  };
-
-  fetch(0);
-  for (int i0 = 0; i0 < N; i0 += KS_ICH) {
+    const uint32_t x = xq[0];
+#pragma unroll
+    for (int d = 0; d < 2; d++)
+#pragma unroll
+      for (int v = 0; v < 4; v++) kr[d][v] = kr[d + 1][v];
+    fetch(min(i + 3, N - 1), kr[2]);
+#pragma unroll
+    for (int d = 0; d < 3; d++) xq[d] = xq[d + 1];
+    xq[3] = x_in[min(i + 4, N - 1)];
     __syncthreads();
-    for (int idx = threadIdx.x; idx < KS8_WAVES * KS8_CB * KS_ICH; idx += 256) {
-      const int k = idx / KS_ICH, ii = idx % KS_ICH;
-      const int64_t c = c0 + k;
-      s_in[k][ii] = (c < B && i0 + ii < N) ? in[c * (N + 1) + i0 + ii] : 0u;
-    }
-    const int iend = min(KS_ICH, N - i0);
-    for (int ii = 0; ii < iend; ii++) {
-      const int i = i0 + ii;
-      const int b = i & 1;
-      build(b);
-      if (i + 1 < N) fetch(i + 1);
-      __syncthreads();
-      const uint32_t* tab = &s_tab[b][0][lane];
-#pragma unroll 8
-      for (int k = 0; k < KS8_CB; k++) {
-        const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[wave * KS8_CB + k][ii]);
-        const uint32_t r = (x + 0x8000u) >> 16;  // round to 16 bits, ties up
-        const uint32_t s0 = tab[(0 * 16 + ((r >> 12) & 15)) * KS_COLS];
-        const uint32_t s1 = tab[(1 * 16 + ((r >> 8) & 15)) * KS_COLS];
-        const uint32_t s2 = tab[(2 * 16 + ((r >> 4) & 15)) * KS_COLS];
-        const uint32_t s3 = tab[(3 * 16 + (r & 15)) * KS_COLS];
-        acc[k] -= (s0 + s1) + (s2 + s3);
-      }
+    const uint32_t r = (x + 0x8000u) >> 16;  // round to 16 bits, ties up
+    const uint32_t* tab = s_tab[b];
+    const uint4* rp[4];
+#pragma unroll
+    for (int p = 0; p < 4; p++)
+      rp[p] = reinterpret_cast<const uint4*>(tab + (p * 16 + ((r >> (12 - 4 * p)) & 15)) * KS8_RS);
+#pragma unroll
+    for (int q = 0; q < KS8_COLS / 4; q++) {
+      const uint4 s0 = rp[0][q], s1 = rp[1][q], s2 = rp[2][q], s3 = rp[3][q];
+      acc[4 * q + 0] -= (s0.x + s1.x) + (s2.x + s3.x);
+      acc[4 * q + 1] -= (s0.y + s1.y) + (s2.y + s3.y);
+      acc[4 * q + 2] -= (s0.z + s1.z) + (s2.z + s3.z);
+      acc[4 * q + 3] -= (s0.w + s1.w) + (s2.w + s3.w);
     }
   }
 
-  if (!col_ok) return;
-#pragma unroll
-  for (int k = 0; k < KS8_CB; k++) {
-    const int64_t c = cw + k;
-    if (c >= B) break;
-    int64_t dst = c;
-    if (mode == kModeRelu) {
-      const int64_t g = gate_begin + c;
-      const int64_t v = g / (bits - 1), bit = g - v * (bits - 1);
-      dst = v * bits + bit;
-    }
-    out[dst * row + col] = acc[k];
+  if (!c_ok) return;
+  int64_t dst = c;
+  if (mode == kModeRelu) {
+    const int64_t g = gate_begin + c;
+    const int64_t v = g / (bits - 1), bit = g - v * (bits - 1);
+    dst = v * bits + bit;
   }
+  uint32_t* o = out + dst * row + col0;
+#pragma unroll
+  for (int j = 0; j < KS8_COLS; j++)
+    if (col0 + j <= n) o[j] = acc[j];
 }
 
 __global__ __launch_bounds__(256) void relu_sign_kernel(uint32_t* __restrict__ y, int n, int32_t bits,
@@ -881,8 +885,7 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
   dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (p.ks_t == 8 && p.ks_basebit == 2) {
-    dim3 g8(static_cast<unsigned>((B + KS8_WAVES * KS8_CB - 1) / (KS8_WAVES * KS8_CB)),
-            static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
+    dim3 g8(static_cast<unsigned>((B + 255) / 256), static_cast<unsigned>((p.n + 1 + KS8_COLS - 1) / KS8_COLS));
     hipLaunchKernelGGL(keyswitch_t8b2_kernel, g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
                        bits, gate_begin);
   } else if (p.ks_t * (1 << p.ks_basebit) <= 32)
