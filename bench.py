@@ -84,7 +84,7 @@ def cpu_baseline(cfg, ca, cb, gpu_out):
 
     p = cfg["params"]
     threads = oracle.threads()
-    count = int(min(64, max(4, 2 * threads)))
+    count = int(min(128, max(8, 6 * threads)))  # about 15 s of oracle work on 16 cores
     keys = oracle.Keys(p, cfg["key_seed"])
     t0 = time.perf_counter()
     ref = oracle.gate_bootstrap(keys, cfg["gate"], ca[:count], cb[:count])
@@ -98,6 +98,182 @@ def cpu_baseline(cfg, ca, cb, gpu_out):
     }
 
 
+def _timed(fn, reps: int):
+    """Median wall time (ms) of fn() over reps calls, each bracketed by HIP
+    events on the current stream (fn launches on that stream)."""
+    import torch
+    times = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    times.sort()
+    return times[len(times) // 2]
+
+
+def suite(path: str):
+    """Throughput of every workload (toy latency, 128-bit NAND batch sweep, MLP
+    and conv ReLU layers, conv ReLU streamed from pinned host memory, 3-bit
+    LUT bootstrap at N = 2048); one JSON record per line, also written to path."""
+    import numpy as np
+    import torch
+
+    from paper_1911_07101_amd import tfhe, workloads as wl
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    recs = []
+
+    def emit(**r):
+        recs.append(r)
+        print(json.dumps(r), flush=True)
+
+    def bits_of(ph):
+        ph = ph.astype(np.int64)
+        return (np.where(ph >= 1 << 31, ph - (1 << 32), ph) > 0).astype(np.uint8)
+
+    # toy: latency of one 16-gate call
+    cfg = wl.CONFIGS["toy"]
+    p = cfg["params"]
+    sk, ek = tfhe.tfhe_keygen_from_seed(p, cfg["key_seed"], 0)
+    a, b = wl.gate_inputs(cfg["input_seed"], cfg["batch"])
+    ca = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0))
+    cb = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), len(a)))
+    out = torch.empty((len(a), p["n"] + 1), dtype=torch.int32, device=dev)
+    ws = tfhe.alloc_workspace(ek, len(a))
+    call = lambda: tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb, out=out, workspace=ws, stream=stream)
+    call()
+    ms = _timed(call, 21)
+    ok = np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(out))), 1 - (a & b))
+    emit(workload="toy", gates=len(a), ms_per_call=ms, per_s=len(a) / ms * 1e3, unit="bootstraps/s", ok=bool(ok))
+    del ek, sk
+
+    # 128-bit NAND: batch sweep
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    sk, ek = tfhe.tfhe_keygen_from_seed(p, cfg["key_seed"], 0)
+    for B in (256, 1024, 4096, 16384, 65536):
+        a, b = wl.gate_inputs(cfg["input_seed"], B)
+        ca = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0))
+        cb = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), B))
+        out = torch.empty((B, p["n"] + 1), dtype=torch.int32, device=dev)
+        ws = tfhe.alloc_workspace(ek, B)
+        call = lambda: tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb, out=out, workspace=ws, stream=stream)
+        call()
+        ms = _timed(call, 5 if B <= 16384 else 3)
+        ok = np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(out))), 1 - (a & b))
+        emit(workload="tfhe128_nand", gates=B, ms_per_call=ms, per_s=B / ms * 1e3, unit="bootstraps/s", ok=bool(ok))
+        del ca, cb, out, ws
+
+    # MLP ReLU: 7680 8-bit values, 53,760 gates in one call
+    cfg = wl.CONFIGS["mlp_relu"]
+    V = cfg["values"]
+    xs = wl.int8_values(cfg["input_seed"], V)
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(xs, 8).ravel()))
+    x = tfhe.to_device(ct.reshape(V, 8, p["n"] + 1))
+    y = torch.empty_like(x)
+    ws = tfhe.alloc_workspace(ek, V * 7)
+    call = lambda: tfhe.glyph_relu_batch(ek, x, 8, y=y, workspace=ws, stream=stream)
+    call()
+    ms = _timed(call, 3)
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(y).reshape(-1, p["n"] + 1))).reshape(V, 8)
+    ok = np.array_equal(wl.from_bits(dec), np.maximum(xs.astype(np.int64), 0))
+    emit(workload="mlp_relu", values=V, gates=V * 7, ms_per_call=ms, per_s=V * 7 / ms * 1e3,
+         unit="gate bootstraps/s", ok=bool(ok))
+    del x, y, ws
+
+    # conv ReLU: 207,360 values, calls of 16,384 gates; inputs resident in HBM
+    cfg = wl.CONFIGS["conv_relu"]
+    V, step = cfg["values"], cfg["gates_per_call"]
+    total = V * 7
+    xs = wl.int8_values(cfg["input_seed"], V)
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(xs, 8).ravel()))
+    ct = ct.reshape(V, 8, p["n"] + 1)
+    x = tfhe.to_device(ct)
+    y = torch.empty_like(x)
+    ws = tfhe.alloc_workspace(ek, step)
+
+    def conv_resident():
+        for begin in range(0, total, step):
+            tfhe.glyph_relu_batch(ek, x, 8, y=y, gate_begin=begin, gate_end=min(begin + step, total),
+                                  workspace=ws, stream=stream)
+    conv_resident()
+    ms = _timed(conv_resident, 1)
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(y).reshape(-1, p["n"] + 1))).reshape(V, 8)
+    ok = np.array_equal(wl.from_bits(dec), np.maximum(xs.astype(np.int64), 0))
+    emit(workload="conv_relu", values=V, gates=total, calls=(total + step - 1) // step, ms=ms,
+         per_s=total / ms * 1e3, unit="gate bootstraps/s", inputs="resident in HBM", ok=bool(ok))
+    del x, y
+
+    # conv ReLU streamed from pinned host memory: chunks of whole values,
+    # copy-in / compute / copy-out on three streams, double-buffered
+    vals = step // 7
+    chunks = [(v0, min(v0 + vals, V)) for v0 in range(0, V, vals)]
+    hx = torch.from_numpy(ct.view(np.int32)).pin_memory()
+    hy = torch.empty(hx.shape, dtype=torch.int32, pin_memory=True)
+    dx = [torch.empty((vals, 8, p["n"] + 1), dtype=torch.int32, device=dev) for _ in range(2)]
+    dy = [torch.empty_like(dx[0]) for _ in range(2)]
+    s_in, s_out = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def conv_streamed():
+        done_in = [torch.cuda.Event() for _ in chunks]
+        done_comp = [torch.cuda.Event() for _ in chunks]
+        done_out = [torch.cuda.Event() for _ in chunks]
+        for k, (v0, v1) in enumerate(chunks):
+            buf = k & 1
+            with torch.cuda.stream(s_in):
+                if k >= 2:
+                    s_in.wait_event(done_comp[k - 2])
+                dx[buf][: v1 - v0].copy_(hx[v0:v1], non_blocking=True)
+                done_in[k].record(s_in)
+            stream.wait_event(done_in[k])
+            if k >= 2:
+                stream.wait_event(done_out[k - 2])
+            tfhe.glyph_relu_batch(ek, dx[buf][: v1 - v0], 8, y=dy[buf][: v1 - v0], workspace=ws, stream=stream)
+            done_comp[k].record(stream)
+            with torch.cuda.stream(s_out):
+                s_out.wait_event(done_comp[k])
+                hy[v0:v1].copy_(dy[buf][: v1 - v0], non_blocking=True)
+                done_out[k].record(s_out)
+        stream.wait_stream(s_out)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    conv_streamed()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, hy.numpy().view(np.uint32).reshape(-1, p["n"] + 1))).reshape(V, 8)
+    ok = np.array_equal(wl.from_bits(dec), np.maximum(xs.astype(np.int64), 0))
+    emit(workload="conv_relu", values=V, gates=total, calls=len(chunks), ms=ms, per_s=total / ms * 1e3,
+         unit="gate bootstraps/s", inputs="pinned host memory, H2D and D2H overlapped with compute",
+         bytes_each_way=int(hx.numel() * 4), ok=bool(ok))
+    del hx, hy, dx, dy, ws, ek, sk
+
+    # 3-bit LUT bootstrap, N = 2048
+    cfg = wl.CONFIGS["lut3_n2048"]
+    p = cfg["params"]
+    sk, ek = tfhe.tfhe_keygen_from_seed(p, cfg["key_seed"], 0)
+    B = cfg["batch"]
+    m = wl.messages(cfg["input_seed"], B, cfg["msg_bits"])
+    table = wl.lut(cfg["input_seed"], cfg["msg_bits"])
+    tv = tfhe.to_device(tfhe.tfhe_lut_testvec(p["N"], cfg["msg_bits"], table))
+    x = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], (m << 28).astype(np.uint32), 0))
+    out = torch.empty((B, p["n"] + 1), dtype=torch.int32, device=dev)
+    ws = tfhe.alloc_workspace(ek, B)
+    call = lambda: tfhe.tfhe_lut_bootstrap_batch(ek, x, tv, out=out, workspace=ws, stream=stream)
+    call()
+    ms = _timed(call, 5)
+    ph = tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(out)).astype(np.int64)
+    ok = np.array_equal(((ph + (1 << 27)) >> 28) & 15, table[m])
+    emit(workload="lut3_n2048", gates=B, ms_per_call=ms, per_s=B / ms * 1e3, unit="bootstraps/s", ok=bool(ok))
+
+    with open(path, "w") as fh:
+        json.dump(recs, fh, indent=1)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,11 +284,17 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="before timing, run one plain device copy of this size (counter calibration)")
+    ap.add_argument("--suite", metavar="PATH", default=None,
+                    help="instead of the headline line, time every workload and write the records to PATH")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the bootstrap batch has no cross-GPU step on this "
               "path; run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.suite:
+        suite(args.suite)
+        return
 
     import numpy as np
     import torch
