@@ -304,32 +304,40 @@ int key_part_shift(int parts) { return parts == 2 ? 16 : 11; }
 
 int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
 
-// Worst-case error of one output coefficient of sum_{r<2l} digit_r * part_r
-// computed with the fp64 transform (forward transform of the digits on the
-// device, key transformed exactly and rounded once, pointwise products and
-// sums, inverse transform).  Radix-2 transform error (Higham, Accuracy and
-// Stability of Numerical Algorithms, Thm 24.2): ||fl(Fx) - Fx||_2 <=
-// m*eta/(1 - m*eta) ||Fx||_2 with eta = mu + gamma4 (sqrt2 + mu), m = log2 n,
-// mu the twiddle error (<= u after one rounding).  With x the folded digits and
-// y a key part (n points), R = 2l products:
-//   ||err||_inf <= R [eps ||x||_2 ||y||_1 + (eps + 3u) ||x||_1 ||y||_2
-//                     + 2u ||x||_1 ||y||_1] + eps ||z||_2
-// where ||x||_2 <= (Bg/2) sqrt(N), ||x||_1 <= (Bg/2) N, likewise for y with
-// the part bound 2^b, and ||z||_2 <= sqrt(N) R N (Bg/2) 2^b.
+// Worst-case error of one output coefficient of z = sum_{r<R} x_r * y_r
+// (R = 2l; x_r the digits, |x| <= D = Bg/2; y_r one key part, |y| <= Y = 2^b)
+// computed as the library does: X_r = fl(F x_r) on the device, K_r = the
+// key's transform F y_r / n computed in long double and rounded once,
+// P = fl(sum_r X_r K_r) pointwise, z^ = fl(G P) with G the unscaled inverse.
+// F is a radix-2 transform of n = N/2 points with F/sqrt(n) unitary, and
+// (Higham, Accuracy and Stability of Numerical Algorithms, Thm 24.2)
+// ||fl(F v) - F v||_2 <= eps ||F v||_2, eps = m eta / (1 - m eta),
+// eta = mu + gamma4 (sqrt2 + mu), m = log2 n, mu <= u the twiddle error.
+// Then, with ||.||_1 of a Hadamard product bounded by Cauchy-Schwarz,
+//   ||z^ - z||_inf <= ||fl(G P) - G P||_2 + ||G (P - P_exact)||_inf
+//                  <= eps (||z||_2 + sqrt(n) E_P) + E_P,
+//   E_P = ||P - P_exact||_1
+//       <= R [eps (1 + u2) + u2 + gamma_2R (1 + eps)(1 + u2)] ||x||_2 ||y||_2
+// (forward error of the digits; key rounding u2 = 2u; a complex product-sum
+// of R terms with two roundings per term and component), ||x||_2 <= D sqrt N,
+// ||y||_2 <= Y sqrt N, and ||z||_2 <= R ||x||_1 ||y||_2 <= R D N Y sqrt N
+// (Young's inequality for the negacyclic convolution).
 double transform_error_bound(const tfhe_params& p, int parts) {
-  const double u = std::ldexp(1.0, -53);
+  const double u = std::ldexp(1.0, -53), u2 = 2 * u;
   const int n = p.N / 2;
   const double m = ilog2(n);
   const double gamma4 = 4 * u / (1 - 4 * u);
   const double eta = u + gamma4 * (std::sqrt(2.0) + u);
   const double eps = m * eta / (1 - m * eta);
   const double R = 2.0 * p.l;
-  const double dig = std::ldexp(1.0, p.bg_bit - 1);
-  const double part = std::ldexp(1.0, key_part_bits(parts));
+  const double g2R = 2 * R * u / (1 - 2 * R * u);
+  const double D = std::ldexp(1.0, p.bg_bit - 1);
+  const double Y = std::ldexp(1.0, key_part_bits(parts));
   const double N = p.N, sN = std::sqrt(N);
-  const double x2 = dig * sN, x1 = dig * N, y2 = part * sN, y1 = part * N;
-  const double z2 = sN * R * N * dig * part;
-  return R * (eps * x2 * y1 + (eps + 3 * u) * x1 * y2 + 2 * u * x1 * y1) + eps * z2;
+  const double x1 = D * N, x2 = D * sN, y2 = Y * sN;
+  const double z2 = R * x1 * y2;
+  const double ep = R * (eps * (1 + u2) + u2 + g2R * (1 + eps) * (1 + u2)) * x2 * y2;
+  return eps * (z2 + std::sqrt(static_cast<double>(n)) * ep) + ep;
 }
 
 int key_parts(const tfhe_params& p) {

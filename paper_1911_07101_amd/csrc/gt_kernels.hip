@@ -311,8 +311,11 @@ struct BrCfg {
   static constexpr int E = Lay::E, T = Lay::T;
   static constexpr int O = 2 * S;       // transform-domain accumulators: (mask, body) x parts
   static constexpr int SHIFT = S == 2 ? 16 : 11;
-  // ciphertexts per block: 256 threads (one wave per ciphertext at N = 1024)
-  static constexpr int CPB = T >= 256 ? 1 : 256 / T;
+  // ciphertexts per block: 256 threads while a ciphertext fits in one wave
+  // (4 per block at N = 1024), else one ciphertext per block (its waves
+  // synchronise between transform passes, and a small block leaves room in
+  // LDS for more of them per CU)
+  static constexpr int CPB = T > 64 ? 1 : 256 / T;
   static constexpr int THREADS = CPB * T;
   static constexpr int SCR = Lay::SCR;
   static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4;

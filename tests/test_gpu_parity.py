@@ -85,9 +85,10 @@ def test_negacyclic_product_exact(torch, N):
     d = rng.integers(-half, half, (B, N)).astype(np.int32)
     b = rng.integers(0, M32, (B, N), dtype=np.uint64).astype(np.uint32)
     # extremes: all digits -Bg/2 against coefficients whose signed key parts
-    # (16-bit halves at N <= 1024, 11-bit thirds at N = 2048) are all at their
-    # largest magnitude with one sign, and alternating digit signs
-    if N <= 1024:
+    # (16-bit halves, or 11-bit thirds where the library needs three parts)
+    # are all at their largest magnitude with one sign, and alternating digit signs
+    parts, _ = tfhe.tfhe_transform_error_bound(p)
+    if parts == 2:
         ext_neg, ext_pos = -(1 << 31), (1 << 31) - (1 << 15)          # halves (-2^15, 0), (2^15, -2^15)
     else:
         ext_neg = -1024 - 1024 * 2**11 - 511 * 2**22                   # thirds (-1024, -1024, -511)

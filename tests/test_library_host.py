@@ -81,7 +81,7 @@ def test_lut_testvec_matches_oracle():
     (dict(N=768), tfhe.TFHE_EUNSUPPORTED),
     (dict(N=4096), tfhe.TFHE_EUNSUPPORTED),
     (dict(l=5, bg_bit=7), tfhe.TFHE_EUNSUPPORTED),         # l * bg_bit > 32
-    (dict(N=2048, l=1, bg_bit=16), tfhe.TFHE_EUNSUPPORTED),  # transform error bound above 1/8
+    (dict(N=2048, l=1, bg_bit=24), tfhe.TFHE_EUNSUPPORTED),  # transform error bound above 1/8
     (dict(ks_t=17, ks_basebit=2), tfhe.TFHE_EUNSUPPORTED),
     (dict(ks_basebit=9, ks_t=2), tfhe.TFHE_EUNSUPPORTED),
     (dict(ks_t=16, ks_basebit=3), tfhe.TFHE_EUNSUPPORTED),    # 128 key rows per coefficient
@@ -114,8 +114,10 @@ def test_transform_error_bound_covers_every_workload():
     _, b8 = tfhe.tfhe_transform_error_bound(dict(TOY, N=1024, bg_bit=8))
     _, b7n = tfhe.tfhe_transform_error_bound(dict(TOY, N=512, bg_bit=7))
     assert b7n < b7 < b8
-    # N = 2048 with 10-bit digits needs the 3-part split
-    assert tfhe.tfhe_transform_error_bound(wl.CONFIGS["lut3_n2048"]["params"])[0] == 3
+    # 16-bit halves cover every workload; 16-bit digits at N = 2048 need the
+    # 3-part split, and 24-bit digits are beyond any split
+    assert all(tfhe.tfhe_transform_error_bound(c["params"])[0] == 2 for c in wl.CONFIGS.values())
+    assert tfhe.tfhe_transform_error_bound(dict(TOY, N=2048, l=1, bg_bit=16))[0] == 3
     with pytest.raises(tfhe.TfheError) as ei:
-        tfhe.tfhe_transform_error_bound(dict(TOY, N=2048, l=1, bg_bit=16))
+        tfhe.tfhe_transform_error_bound(dict(TOY, N=2048, l=1, bg_bit=24))
     assert ei.value.rc == tfhe.TFHE_EUNSUPPORTED
