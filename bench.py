@@ -116,8 +116,9 @@ def _timed(fn, reps: int):
 
 def suite(path: str):
     """Throughput of every workload (toy latency, 128-bit NAND batch sweep, MLP
-    and conv ReLU layers, conv ReLU streamed from pinned host memory, 3-bit
-    LUT bootstrap at N = 2048); one JSON record per line, also written to path."""
+    forward ReLU and backward iReLU, conv ReLU resident and streamed from
+    pinned host memory, 3-bit LUT bootstrap at N = 2048); one JSON record per
+    line, also written to path."""
     import numpy as np
     import torch
 
@@ -184,6 +185,26 @@ def suite(path: str):
     emit(workload="mlp_relu", values=V, gates=V * 7, ms_per_call=ms, per_s=V * 7 / ms * 1e3,
          unit="gate bootstraps/s", ok=bool(ok))
     del x, y, ws
+
+    # MLP backward iReLU: 7680 8-bit errors gated by the forward signs
+    cfg = wl.CONFIGS["mlp_irelu"]
+    V = cfg["values"]
+    us = wl.int8_values(cfg["input_seed"], V)
+    ds = wl.int8_values(cfg["input_seed"], V, stream=7)
+    u = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(us, 8).ravel()))
+                       .reshape(V, 8, p["n"] + 1))
+    d = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"] + 1, tfhe.encode_bits(wl.to_bits(ds, 8).ravel()))
+                       .reshape(V, 8, p["n"] + 1))
+    y = torch.empty_like(d)
+    ws = tfhe.alloc_workspace(ek, V * 8)
+    call = lambda: tfhe.glyph_irelu_batch(ek, u, d, out=y, workspace=ws, stream=stream)
+    call()
+    ms = _timed(call, 3)
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(y).reshape(-1, p["n"] + 1))).reshape(V, 8)
+    ok = np.array_equal(wl.from_bits(dec), np.where(us >= 0, ds.astype(np.int64), 0))
+    emit(workload="mlp_irelu", values=V, gates=V * 8, ms_per_call=ms, per_s=V * 8 / ms * 1e3,
+         unit="gate bootstraps/s", ok=bool(ok))
+    del u, d, y, ws
 
     # conv ReLU: 207,360 values, calls of 16,384 gates; inputs resident in HBM
     cfg = wl.CONFIGS["conv_relu"]

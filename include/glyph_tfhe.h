@@ -189,6 +189,21 @@ int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, in
                      int32_t bits, int64_t gate_begin, int64_t gate_end, void* workspace,
                      int64_t workspace_bytes, void* stream);
 
+/* Glyph backward iReLU unit (Section 3.1, "Backward iReLU"): the error of
+ * the layer below is the error delta where the forward pre-activation u was
+ * non-negative, and zero where it was negative.  u: [V][u_bits][n+1] device
+ * (the forward input; only its sign word, bit u_bits-1, is read); delta,
+ * out: [V][bits][n+1] device, two's complement LSB first.  Output bit i of
+ * value v is AND(NOT u[v][u_bits-1], delta[v][i]) for every i < bits -- the
+ * error's sign bit included, so a negative error becomes 0 where u < 0 (the
+ * paper counts bits-1 AND gates for the unit; the sign bit needs one too).
+ * Gate g is bit g % bits of value g / bits; a call computes gates
+ * [gate_begin, gate_end) and writes exactly their output words.  out must
+ * not alias u or delta. */
+int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits, const uint32_t* delta,
+                      uint32_t* out, int64_t V, int32_t bits, int64_t gate_begin, int64_t gate_end,
+                      void* workspace, int64_t workspace_bytes, void* stream);
+
 /* NOT without bootstrapping (Section 3.1): out = -in word by word.
  * in, out: [count][dim+1] device. */
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);

@@ -311,6 +311,27 @@ def relu(keys: Keys, x, bits):
     return y
 
 
+def irelu_gates(keys: Keys, u, u_bits, delta, bits, gate_ids):
+    """Outputs of the given gates of the backward iReLU (Section 3.1,
+    "Backward iReLU"): gate g is bit i = g % bits of value v = g // bits,
+    AND(NOT u[v][u_bits-1], delta[v][i]) -- the error bit where the forward
+    pre-activation's sign is 0, else 0.  Every bit of the error is gated, the
+    sign bit included."""
+    p = keys.p
+    u = np.ascontiguousarray(u, dtype=np.uint32).reshape(-1, u_bits, p.n + 1)
+    delta = np.ascontiguousarray(delta, dtype=np.uint32).reshape(-1, bits, p.n + 1)
+    ids = np.asarray(gate_ids, dtype=np.int64)
+    v, i = ids // bits, ids % bits
+    return gate_bootstrap(keys, "ANDNY", u[v, u_bits - 1], delta[v, i])
+
+
+def irelu(keys: Keys, u, u_bits, delta, bits):
+    """Full backward iReLU over delta[V][bits][n+1]."""
+    p = keys.p
+    V = np.asarray(delta).size // (bits * (p.n + 1))
+    return irelu_gates(keys, u, u_bits, delta, bits, np.arange(V * bits)).reshape(V, bits, p.n + 1)
+
+
 def not_gate(ct):
     ct = np.ascontiguousarray(ct, dtype=np.uint32)
     return (np.uint32(0) - ct).astype(np.uint32)

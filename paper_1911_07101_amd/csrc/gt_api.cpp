@@ -429,6 +429,24 @@ int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, in
   return launch_relu_sign(ek, y, bits, v_begin, v_end, stream);
 }
 
+int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits, const uint32_t* delta,
+                      uint32_t* out, int64_t V, int32_t bits, int64_t gate_begin, int64_t gate_end,
+                      void* workspace, int64_t workspace_bytes_, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (V < 0 || bits < 1 || bits > 64 || u_bits < 1 || u_bits > 64)
+    return fail(TFHE_EINVAL, "need V >= 0, 1 <= bits <= 64 and 1 <= u_bits <= 64");
+  const int64_t total = V * bits;
+  if (gate_begin < 0 || gate_end < gate_begin || gate_end > total)
+    return fail(TFHE_EINVAL, "gate window [%lld, %lld) outside [0, %lld)", static_cast<long long>(gate_begin),
+                static_cast<long long>(gate_end), static_cast<long long>(total));
+  const int64_t B = gate_end - gate_begin;
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(u, "u")) || (rc = check_u32(delta, "delta")) || (rc = check_u32(out, "out"))) return rc;
+  PrepArgs a{kModeIRelu, TFHE_ANDNY, u, delta, B, bits, gate_begin, u_bits};
+  return bootstrap_common(ek, a, nullptr, out, kModeIRelu, workspace, workspace_bytes_, stream, true);
+}
+
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {
   if (dim < 1 || count < 0) return fail(TFHE_EINVAL, "need dim >= 1 and count >= 0");
   if (count == 0) return TFHE_OK;

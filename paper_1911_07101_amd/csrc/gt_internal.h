@@ -60,16 +60,17 @@ struct Workspace {
 int64_t workspace_bytes(const tfhe_params& p, int64_t B);
 Workspace carve_workspace(const tfhe_params& p, void* ws, int64_t B);
 
-enum InputMode : int { kModeGate = 0, kModePlain = 1, kModeRelu = 2 };
+enum InputMode : int { kModeGate = 0, kModePlain = 1, kModeRelu = 2, kModeIRelu = 3 };
 
 struct PrepArgs {
   int mode;
   int gate;
-  const uint32_t* ca;  // gate: first operand; plain: the input; relu: x
-  const uint32_t* cb;  // gate: second operand
+  const uint32_t* ca;  // gate: first operand; plain: the input; relu: x; irelu: u
+  const uint32_t* cb;  // gate: second operand; irelu: delta
   int64_t B;
-  int32_t bits;        // relu
-  int64_t gate_begin;  // relu
+  int32_t bits;        // relu: bits of x; irelu: bits of delta
+  int64_t gate_begin;  // relu, irelu
+  int32_t sign_bits;   // irelu: bits of u (its sign is bit sign_bits - 1)
 };
 
 int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws, void* stream);

@@ -272,8 +272,8 @@ __device__ __forceinline__ GateCoef gate_coef(int gate) {
 
 __global__ __launch_bounds__(256) void prep_kernel(int mode, int gate, const uint32_t* __restrict__ ca,
                                                    const uint32_t* __restrict__ cb, int n, int N,
-                                                   int64_t B, int32_t bits, int64_t gate_begin,
-                                                   uint16_t* __restrict__ abar) {
+                                                   int64_t B, int32_t bits, int32_t sign_bits,
+                                                   int64_t gate_begin, uint16_t* __restrict__ abar) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const int64_t total = B * (n + 1);
   if (idx >= total) return;
@@ -290,11 +290,16 @@ __global__ __launch_bounds__(256) void prep_kernel(int mode, int gate, const uin
       const int64_t v = g / (bits - 1), i = g - v * (bits - 1);
       pa = ca + (v * bits + (bits - 1)) * (n + 1);  // sign bit
       pb = ca + (v * bits + i) * (n + 1);
+    } else if (mode == kModeIRelu) {
+      const int64_t g = gate_begin + c;
+      const int64_t v = g / bits;
+      pa = ca + (v * sign_bits + (sign_bits - 1)) * (n + 1);  // sign bit of u
+      pb = cb + g * (n + 1);                                   // error bit g % bits of value v
     } else {
       pa = ca + c * (n + 1);
       pb = cb + c * (n + 1);
     }
-    const GateCoef gc = gate_coef(mode == kModeRelu ? static_cast<int>(TFHE_ANDNY) : gate);
+    const GateCoef gc = gate_coef(mode == kModeGate ? gate : static_cast<int>(TFHE_ANDNY));
     x = static_cast<uint32_t>(gc.wa) * pa[k] + static_cast<uint32_t>(gc.wb) * pb[k] +
         (k == n ? gc.konst : 0u);
   }
@@ -496,6 +501,18 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
 }
 
 // ------------------------------------------------------- key switching
+// Output sample of batch entry c: c itself, or for the activation units the
+// gate's place in the [V][bits] output tensor (forward ReLU: bit
+// g % (bits-1) of value g / (bits-1); backward iReLU: entry g of [V][bits]).
+__device__ __forceinline__ int64_t out_index(int mode, int64_t c, int32_t bits, int64_t gate_begin) {
+  const int64_t g = gate_begin + c;
+  if (mode == kModeRelu) {
+    const int64_t v = g / (bits - 1);
+    return v * bits + (g - v * (bits - 1));
+  }
+  return mode == kModeIRelu ? g : c;
+}
+
 // One wave per block covers 64 output columns of KS_CB samples.  Each lane
 // keeps the running output word of its column for every sample.  For each
 // input coefficient i the block stages the key rows of all t digits and all
@@ -605,13 +622,7 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
   for (int k = 0; k < KS_CB; k++) {
     const int64_t c = c0 + k;
     if (c >= B) break;
-    int64_t dst = c;
-    if (mode == kModeRelu) {
-      const int64_t g = gate_begin + c;
-      const int64_t v = g / (bits - 1), bit = g - v * (bits - 1);
-      dst = v * bits + bit;
-    }
-    out[dst * row + col] = acc[k];
+    out[out_index(mode, c, bits, gate_begin) * row + col] = acc[k];
   }
 }
 
@@ -706,13 +717,7 @@ __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __r
   }
 
   if (!c_ok) return;
-  int64_t dst = c;
-  if (mode == kModeRelu) {
-    const int64_t g = gate_begin + c;
-    const int64_t v = g / (bits - 1), bit = g - v * (bits - 1);
-    dst = v * bits + bit;
-  }
-  uint32_t* o = out + dst * row + col0;
+  uint32_t* o = out + out_index(mode, c, bits, gate_begin) * row + col0;
 #pragma unroll
   for (int j = 0; j < KS8_COLS; j++)
     if (col0 + j <= n) o[j] = acc[j];
@@ -870,7 +875,7 @@ int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws,
   const int64_t blocks = (total + 255) / 256;
   hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), a.mode, a.gate, a.ca, a.cb, ek->p.n, ek->p.N,
-                     a.B, a.bits, a.gate_begin, ws.abar);
+                     a.B, a.bits, a.sign_bits, a.gate_begin, ws.abar);
   return launch_status("prep_kernel");
 }
 

@@ -66,6 +66,7 @@ _SIGNATURES = {
     "tfhe_bootstrap_extract_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
     "tfhe_keyswitch_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp]),
     "glyph_relu_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
+    "glyph_irelu_batch": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
@@ -307,6 +308,21 @@ def glyph_relu_batch(ek: EvalKey, x, bits: int, y=None, gate_begin: int = 0, gat
     _check(lib().glyph_relu_batch(ek.handle, _dptr(x), _dptr(y), V, bits, gate_begin, gate_end,
                                   _dptr(ws), ws.numel(), _stream(stream)))
     return y
+
+
+def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate_end=None,
+                      workspace=None, stream=None):
+    """Backward iReLU: u [V][u_bits][n+1] (its sign words are read), delta and
+    out [V][bits][n+1]; gates [gate_begin, gate_end) of the V*bits."""
+    V, u_bits = u.shape[0], u.shape[1]
+    bits = delta.shape[1]
+    out = _empty(tuple(delta.shape), ek) if out is None else out
+    if gate_end is None:
+        gate_end = V * bits
+    ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
+    _check(lib().glyph_irelu_batch(ek.handle, _dptr(u), u_bits, _dptr(delta), _dptr(out), V, bits,
+                                   gate_begin, gate_end, _dptr(ws), ws.numel(), _stream(stream)))
+    return out
 
 
 def tfhe_not_batch(x, out=None, stream=None):

@@ -36,6 +36,10 @@ CONFIGS = {
     "conv_relu": dict(params=_TFHE_1024, kind="relu", values=60 * 6 * 24 * 24, bits=8,
                       gates_per_call=16384, key_seed=0x19110713, input_seed=0x5EED0004,
                       sample=64),
+    # backward iReLU of the MLP layer: 8-bit errors gated by the signs of the
+    # forward 8-bit pre-activations
+    "mlp_irelu": dict(params=_TFHE_1024, kind="irelu", values=60 * 128, bits=8,
+                      key_seed=0x19110715, input_seed=0x5EED0006, sample=64),
     # programmable (table-lookup) bootstrap on 3-bit messages, N = 2048
     "lut3_n2048": dict(params=dict(n=750, N=2048, l=2, bg_bit=10, ks_t=8, ks_basebit=2,
                                    alpha_lwe=2.0 ** -17, alpha_bk=2.0 ** -45,
@@ -59,9 +63,10 @@ def gate_inputs(seed: int, batch: int):
     return random_bits(seed, batch, 1), random_bits(seed, batch, 2)
 
 
-def int8_values(seed: int, count: int) -> np.ndarray:
-    """count values uniform in [-128, 127]."""
-    return _rng(seed, 3).integers(-128, 128, size=count, dtype=np.int64).astype(np.int8)
+def int8_values(seed: int, count: int, stream: int = 3) -> np.ndarray:
+    """count values uniform in [-128, 127] (stream 3: activations; another
+    stream gives an independent set, e.g. 7 for backward errors)."""
+    return _rng(seed, stream).integers(-128, 128, size=count, dtype=np.int64).astype(np.int8)
 
 
 def to_bits(values: np.ndarray, bits: int) -> np.ndarray:

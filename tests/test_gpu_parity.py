@@ -217,6 +217,43 @@ def test_relu_toy_all_values(torch):
     assert np.array_equal(wl.from_bits(dec), np.maximum(xs, 0))
 
 
+def test_irelu_toy_all_4bit_pairs(torch):
+    """Backward iReLU for every (4-bit u, 4-bit delta) pair on the toy
+    parameters, in uneven gate windows: bit-exact with the oracle, and every
+    output decrypts to delta where u >= 0, else 0."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    us, ds = np.meshgrid(np.arange(-8, 8), np.arange(-8, 8), indexing="ij")
+    us, ds = us.ravel(), ds.ravel()
+    V = len(us)
+    cu = tfhe.tfhe_encrypt_torus(sk, 31, tfhe.encode_bits(wl.to_bits(us, 4).ravel())).reshape(V, 4, p["n"] + 1)
+    cd = tfhe.tfhe_encrypt_torus(sk, 32, tfhe.encode_bits(wl.to_bits(ds, 4).ravel())).reshape(V, 4, p["n"] + 1)
+    u, d = tfhe.to_device(cu), tfhe.to_device(cd)
+    y = torch.zeros_like(d)
+    say(f"irelu toy {V} pairs in 3 windows")
+    for s, e in [(0, 3), (3, 700), (700, V * 4)]:
+        tfhe.glyph_irelu_batch(ek, u, d, out=y, gate_begin=s, gate_end=e)
+    got = tfhe.to_host(y)
+    assert np.array_equal(got, oracle.irelu(ok, cu, 4, cd, 4))
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(V, 4)
+    assert np.array_equal(wl.from_bits(dec), np.where(us >= 0, ds, 0))
+
+
+def test_irelu_window_writes_only_its_gates(torch):
+    """A call writes exactly the output words of its gate window."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    V, bits = 9, 5
+    rng = np.random.default_rng(5)
+    cu = tfhe.tfhe_encrypt_torus(sk, 33, tfhe.encode_bits(rng.integers(0, 2, V * 3))).reshape(V, 3, p["n"] + 1)
+    cd = tfhe.tfhe_encrypt_torus(sk, 34, tfhe.encode_bits(rng.integers(0, 2, V * bits))).reshape(V, bits, p["n"] + 1)
+    y = torch.full((V, bits, p["n"] + 1), -1, dtype=torch.int32, device="cuda:0")
+    tfhe.glyph_irelu_batch(ek, tfhe.to_device(cu), tfhe.to_device(cd), out=y, gate_begin=7, gate_end=23)
+    got = tfhe.to_host(y).reshape(V * bits, p["n"] + 1)
+    assert np.all(got[:7] == M32 - 1) and np.all(got[23:] == M32 - 1)
+    assert np.array_equal(got[7:23], oracle.irelu_gates(ok, cu, 3, cd, bits, np.arange(7, 23)))
+
+
 # ---------------------------------------------------- full-size workloads
 
 def test_tfhe128_nand_4096(torch):
@@ -257,6 +294,36 @@ def test_mlp_relu_7680(torch):
     got = np.stack([y[g // 7, g % 7] for g in gates])
     assert np.array_equal(got, ref)
     assert np.all(y[:, 7, :p["n"]] == 0) and np.all(y[:, 7, p["n"]] == M32 - MU)
+
+
+def test_mlp_irelu_7680(torch):
+    """Backward iReLU over the MLP layer: 7680 8-bit errors gated by the
+    signs of the 7680 forward pre-activations, 61,440 gates in windows of
+    16,384 (the last one ragged)."""
+    cfg = wl.CONFIGS["mlp_irelu"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)  # same parameter set, shared keys
+    V = cfg["values"]
+    us = wl.int8_values(cfg["input_seed"], V)
+    ds = wl.int8_values(cfg["input_seed"], V, stream=7)
+    cu = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(us, 8).ravel()))
+    cd = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"] + 1, tfhe.encode_bits(wl.to_bits(ds, 8).ravel()))
+    cu, cd = cu.reshape(V, 8, p["n"] + 1), cd.reshape(V, 8, p["n"] + 1)
+    u, d = tfhe.to_device(cu), tfhe.to_device(cd)
+    y = torch.empty_like(d)
+    total, step = V * 8, 16384
+    ws = tfhe.alloc_workspace(ek, step)
+    say(f"irelu n=630 V={V} gates={total}")
+    t0 = time.time()
+    for s in range(0, total, step):
+        tfhe.glyph_irelu_batch(ek, u, d, out=y, gate_begin=s, gate_end=min(s + step, total), workspace=ws)
+    got = tfhe.to_host(y)
+    say(f"  gpu {time.time() - t0:.2f}s")
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(V, 8)
+    assert np.array_equal(wl.from_bits(dec), np.where(us >= 0, ds.astype(np.int64), 0))
+    gates = wl.sample_indices(cfg["input_seed"], total, cfg["sample"])
+    ref = oracle.irelu_gates(ok, cu, 8, cd, 8, gates)
+    assert np.array_equal(got.reshape(-1, p["n"] + 1)[gates], ref)
 
 
 def test_conv_relu_streamed(torch):
