@@ -117,8 +117,9 @@ def _timed(fn, reps: int):
 def suite(path: str):
     """Throughput of every workload (toy latency, 128-bit NAND batch sweep, MLP
     forward ReLU and backward iReLU, conv ReLU resident and streamed from
-    pinned host memory, 3-bit LUT bootstrap at N = 2048); one JSON record per
-    line, also written to path."""
+    pinned host memory, the 3-bit softmax unit as a multiplexer tree and as a
+    LUT bootstrap at N = 2048); one JSON record per line, also written to
+    path."""
     import numpy as np
     import torch
 
@@ -271,7 +272,27 @@ def suite(path: str):
     emit(workload="conv_relu", values=V, gates=total, calls=len(chunks), ms=ms, per_s=total / ms * 1e3,
          unit="gate bootstraps/s", inputs="pinned host memory, H2D and D2H overlapped with compute",
          bytes_each_way=int(hx.numel() * 4), ok=bool(ok))
-    del hx, hy, dx, dy, ws, ek, sk
+    del hx, hy, dx, dy, ws
+
+    # the paper's 3-bit softmax unit as a multiplexer tree over bit-wise
+    # encrypted inputs (same messages and table as the LUT bootstrap below)
+    cfg = wl.CONFIGS["softmax_mux3"]
+    V, mb, ob = cfg["values"], cfg["msg_bits"], cfg["out_bits"]
+    m = wl.messages(cfg["input_seed"], V, mb)
+    table = wl.lut(cfg["input_seed"], mb)
+    x = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(m, mb).ravel()))
+                       .reshape(V, mb, p["n"] + 1))
+    y = torch.empty((V, ob, p["n"] + 1), dtype=torch.int32, device=dev)
+    ws = tfhe.alloc_mux_lut_workspace(ek, V, mb, ob)
+    call = lambda: tfhe.glyph_mux_lut_batch(ek, x, table, ob, out=y, workspace=ws, stream=stream)
+    call()
+    ms = _timed(call, 3)
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(y).reshape(-1, p["n"] + 1))).reshape(V, ob)
+    ok = np.array_equal((dec.astype(np.int64) << np.arange(ob)).sum(axis=1), table[m])
+    muxes = ((1 << (mb - 1)) - 1) * ob
+    emit(workload="softmax_mux3", values=V, multiplexers_per_value=muxes, bootstraps=2 * muxes * V,
+         ms_per_call=ms, per_s=V / ms * 1e3, unit="3-bit lookups/s", ok=bool(ok))
+    del x, y, ws, ek, sk
 
     # 3-bit LUT bootstrap, N = 2048
     cfg = wl.CONFIGS["lut3_n2048"]
@@ -289,7 +310,8 @@ def suite(path: str):
     ms = _timed(call, 5)
     ph = tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(out)).astype(np.int64)
     ok = np.array_equal(((ph + (1 << 27)) >> 28) & 15, table[m])
-    emit(workload="lut3_n2048", gates=B, ms_per_call=ms, per_s=B / ms * 1e3, unit="bootstraps/s", ok=bool(ok))
+    emit(workload="lut3_n2048", gates=B, ms_per_call=ms, per_s=B / ms * 1e3, unit="bootstraps/s = 3-bit lookups/s",
+         ok=bool(ok))
 
     with open(path, "w") as fh:
         json.dump(recs, fh, indent=1)

@@ -204,6 +204,36 @@ int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits
                       uint32_t* out, int64_t V, int32_t bits, int64_t gate_begin, int64_t gate_end,
                       void* workspace, int64_t workspace_bytes, void* stream);
 
+/* TFHE homomorphic multiplexer, the building block of the paper's softmax
+ * unit (Section 3.1, "Forward Softmax"): out[e] encrypts c[e] ? a[e] : b[e]
+ * for encrypted bits.  Each multiplexer takes two bootstraps without key
+ * switching -- AND(c, a) and AND(NOT c, b) -- whose dimension-N results are
+ * added with the constant 1/8 (at most one of them is true) and key-switched
+ * once.  c, a, b, out: [B][n+1] device; the workspace must hold
+ * tfhe_workspace_bytes(ek, 2 * B). */
+int tfhe_mux_batch(const tfhe_eval_key* ek, const uint32_t* c, const uint32_t* a, const uint32_t* b,
+                   uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes, void* stream);
+
+/* Table lookup by a tree of multiplexers, the paper's 3-bit softmax
+ * exponentiation unit (Section 3.1, "Forward Softmax", generalised): value v
+ * is msg_bits encrypted bits x[v][0..msg_bits) (LSB first) selecting entry
+ * k = sum x[v][i] 2^i of the public table[2^msg_bits] (host memory, entries
+ * below 2^out_bits); out[v][o] encrypts bit o of table[k].  The first tree
+ * level selects between two constants with x[v][0] and needs no bootstrap
+ * (its node is a constant, x[v][0] or NOT x[v][0]); each further level is
+ * one batch of multiplexers over all values, output bits and nodes:
+ * (2^(msg_bits-1) - 1) * out_bits multiplexers per value.  x:
+ * [V][msg_bits][n+1], out: [V][out_bits][n+1] device; 1 <= msg_bits <= 6,
+ * 1 <= out_bits <= 32; the workspace must hold
+ * glyph_mux_lut_workspace_bytes(ek, V, msg_bits, out_bits) bytes. */
+int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits, const uint32_t* table,
+                        int32_t out_bits, uint32_t* out, int64_t V, void* workspace,
+                        int64_t workspace_bytes, void* stream);
+
+/* Workspace bytes of glyph_mux_lut_batch (negative error code on bad input). */
+int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_t msg_bits,
+                                      int32_t out_bits);
+
 /* NOT without bootstrapping (Section 3.1): out = -in word by word.
  * in, out: [count][dim+1] device. */
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);

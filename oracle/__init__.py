@@ -2,8 +2,9 @@
 
 The oracle is a plain, slow CPU implementation of TFHE gate bootstrapping
 (modulus switch, blind rotation with schoolbook negacyclic products, sample
-extraction, key switching), the Glyph forward ReLU unit and the look-up-table
-bootstrap.  Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
+extraction, key switching), the Glyph forward ReLU and backward iReLU units,
+the homomorphic multiplexer and the softmax's multiplexer-tree table lookup,
+and the look-up-table bootstrap.  Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 ``cpu_baseline`` leg may import this package; the GPU library never does, and
 the two share no code.
 """
@@ -330,6 +331,62 @@ def irelu(keys: Keys, u, u_bits, delta, bits):
     p = keys.p
     V = np.asarray(delta).size // (bits * (p.n + 1))
     return irelu_gates(keys, u, u_bits, delta, bits, np.arange(V * bits)).reshape(V, bits, p.n + 1)
+
+
+def mux(keys: Keys, c, a, b):
+    """Homomorphic multiplexer c ? a : b on encrypted bits (the unit of the
+    softmax lookup, Section 3.1 "Forward Softmax"): bootstrap AND(c, a) and
+    AND(NOT c, b) to dimension N without key switching, add the two samples
+    and the constant 1/8 (true + false + 1/8 = 1/8, false + false + 1/8 =
+    -1/8), then key-switch once."""
+    p = keys.p
+    c = np.asarray(c, dtype=np.uint32).reshape(-1, p.n + 1)
+    a = np.asarray(a, dtype=np.uint32).reshape(-1, p.n + 1)
+    b = np.asarray(b, dtype=np.uint32).reshape(-1, p.n + 1)
+    M = len(c)
+    halves = [gate_combine(p, "AND", c[e], a[e]) for e in range(M)]
+    halves += [gate_combine(p, "ANDNY", c[e], b[e]) for e in range(M)]
+    ext = bootstrap_no_ks(keys, np.stack(halves), gate_testvec(p.N))
+    s = (ext[:M].astype(np.uint64) + ext[M:].astype(np.uint64)) & 0xFFFFFFFF
+    s[:, p.N] = (s[:, p.N] + MU) & 0xFFFFFFFF
+    return keyswitch(keys, s.astype(np.uint32))
+
+
+def mux_lut(keys: Keys, x, msg_bits, table, out_bits):
+    """Table lookup by a tree of multiplexers (the paper's softmax
+    exponentiation unit): x[v] holds msg_bits encrypted bits, LSB first,
+    selecting entry k = sum x[v][i] 2^i of the public table; the result holds
+    the out_bits bits of table[k].  Tree level 1 picks between constants with
+    x[v][0] (a constant, x[v][0] or NOT x[v][0], no bootstrap); level i picks
+    between the level i-1 nodes 2j (bit 0) and 2j + 1 (bit 1) with x[v][i-1]."""
+    p = keys.p
+    x = np.asarray(x, dtype=np.uint32).reshape(-1, msg_bits, p.n + 1)
+    table = np.asarray(table, dtype=np.int64)
+    V = len(x)
+    triv = lambda bit: np.concatenate([np.zeros(p.n, np.uint32),
+                                       np.array([MU if bit else (1 << 32) - MU], np.uint32)])
+    # nodes[v][o] = list of ciphertexts of the current level
+    nodes = [[None] * out_bits for _ in range(V)]
+    for v in range(V):
+        for o in range(out_bits):
+            lvl = []
+            for j in range(1 << (msg_bits - 1)):
+                b0, b1 = (table[2 * j] >> o) & 1, (table[2 * j + 1] >> o) & 1
+                lvl.append(triv(b0) if b0 == b1 else (x[v][0].copy() if b1 else not_gate(x[v][0])))
+            nodes[v][o] = lvl
+    for level in range(1, msg_bits):
+        sel, ta, fb, where = [], [], [], []
+        for v in range(V):
+            for o in range(out_bits):
+                for j in range(len(nodes[v][o]) // 2):
+                    sel.append(x[v][level]); ta.append(nodes[v][o][2 * j + 1]); fb.append(nodes[v][o][2 * j])
+                    where.append((v, o))
+        res = mux(keys, np.stack(sel), np.stack(ta), np.stack(fb))
+        new = [[[] for _ in range(out_bits)] for _ in range(V)]
+        for (v, o), r in zip(where, res):
+            new[v][o].append(r)
+        nodes = new
+    return np.stack([np.stack([nodes[v][o][0] for o in range(out_bits)]) for v in range(V)])
 
 
 def not_gate(ct):

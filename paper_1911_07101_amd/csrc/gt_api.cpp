@@ -447,6 +447,119 @@ int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits
   return bootstrap_common(ek, a, nullptr, out, kModeIRelu, workspace, workspace_bytes_, stream, true);
 }
 
+// Multiplexers: a.B = 2M samples (the two halves of M multiplexers) are
+// prepared and blind-rotated with the gate polynomial, the halves of each
+// multiplexer are added with (0, 1/8) and the M sums key-switched into out.
+static int mux_common(const tfhe_eval_key* ek, const PrepArgs& a, uint32_t* out, void* ws, int64_t ws_bytes,
+                      void* stream) {
+  int rc = check_ws(ek, ws, ws_bytes, a.B);
+  if (rc) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  Workspace w = carve_workspace(ek->p, ws, a.B);
+  const int64_t M = a.B / 2;
+  {
+    StageScope sc(0, stream);
+    if ((rc = launch_prep(ek, a, w, stream))) return rc;
+  }
+  {
+    StageScope sc(1, stream);
+    if ((rc = launch_blind_rotate(ek, w, nullptr, a.B, stream))) return rc;
+    if ((rc = launch_mux_combine(ek, w.extract, M, stream))) return rc;
+  }
+  StageScope sc(2, stream);
+  return launch_keyswitch(ek, w.extract, out, M, kModePlain, 0, 0, stream);
+}
+
+int tfhe_mux_batch(const tfhe_eval_key* ek, const uint32_t* c, const uint32_t* a, const uint32_t* b,
+                   uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(c, "c")) || (rc = check_u32(a, "a")) || (rc = check_u32(b, "b")) ||
+      (rc = check_u32(out, "out")))
+    return rc;
+  PrepArgs pa{};
+  pa.mode = kModeMux;
+  pa.ca = c;
+  pa.cb = a;
+  pa.cc = b;
+  pa.B = 2 * B;
+  return mux_common(ek, pa, out, workspace, workspace_bytes_, stream);
+}
+
+// Workspace of glyph_mux_lut_batch: the tree's first two levels of nodes and
+// the bootstrap workspace of its widest bootstrapped level.
+struct MuxLutLayout {
+  int64_t a_off, b_off, ws_off, total, nodes_a, nodes_b, widest;
+};
+
+static MuxLutLayout mux_lut_layout(const tfhe_params& p, int64_t V, int32_t msg_bits, int32_t out_bits) {
+  MuxLutLayout L{};
+  const int64_t row = (p.n + 1) * 4;
+  L.nodes_a = msg_bits >= 2 ? V * out_bits * (int64_t{1} << (msg_bits - 1)) : 0;
+  L.nodes_b = msg_bits >= 3 ? V * out_bits * (int64_t{1} << (msg_bits - 2)) : 0;
+  L.widest = msg_bits >= 2 ? 2 * V * out_bits * (int64_t{1} << (msg_bits - 2)) : 0;
+  auto up = [](int64_t x) { return (x + 255) / 256 * 256; };
+  L.a_off = 0;
+  L.b_off = up(L.nodes_a * row);
+  L.ws_off = L.b_off + up(L.nodes_b * row);
+  L.total = L.ws_off + (L.widest ? workspace_bytes(p, L.widest) : 0);
+  return L;
+}
+
+int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_t msg_bits, int32_t out_bits) {
+  if (!ek || V < 0 || msg_bits < 1 || msg_bits > 6 || out_bits < 1 || out_bits > 32)
+    return fail(TFHE_EINVAL, "bad argument to glyph_mux_lut_workspace_bytes");
+  return mux_lut_layout(ek->p, V, msg_bits, out_bits).total;
+}
+
+int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits, const uint32_t* table,
+                        int32_t out_bits, uint32_t* out, int64_t V, void* workspace, int64_t workspace_bytes_,
+                        void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (V < 0 || msg_bits < 1 || msg_bits > 6 || out_bits < 1 || out_bits > 32)
+    return fail(TFHE_EINVAL, "need V >= 0, 1 <= msg_bits <= 6, 1 <= out_bits <= 32");
+  if (!table) return fail(TFHE_EINVAL, "NULL table");
+  for (int k = 0; k < (1 << msg_bits); k++)
+    if (out_bits < 32 && (table[k] >> out_bits) != 0)
+      return fail(TFHE_EINVAL, "table entry %d does not fit in %d bits", k, out_bits);
+  if (V == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(x, "x")) || (rc = check_u32(out, "out"))) return rc;
+  const MuxLutLayout L = mux_lut_layout(ek->p, V, msg_bits, out_bits);
+  if (!workspace) return fail(TFHE_EINVAL, "workspace is NULL");
+  if (!aligned(workspace, 256)) return fail(TFHE_EINVAL, "workspace must be 256-byte aligned");
+  if (workspace_bytes_ < L.total)
+    return fail(TFHE_EINVAL, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                static_cast<long long>(workspace_bytes_), static_cast<long long>(L.total));
+  char* base = static_cast<char*>(workspace);
+  uint32_t* nodes[2] = {reinterpret_cast<uint32_t*>(base + L.a_off), reinterpret_cast<uint32_t*>(base + L.b_off)};
+  {
+    DeviceGuard g(ek->device);
+    if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+    if ((rc = launch_lut_leaf(ek, x, msg_bits, table, out_bits, V, msg_bits == 1 ? out : nodes[0], stream)))
+      return rc;
+  }
+  // levels 2 .. msg_bits: level k reads the nodes of level k-1 and writes
+  // 2^(msg_bits-k) nodes per (value, output bit), the last level into out
+  for (int k = 2; k <= msg_bits; k++) {
+    PrepArgs pa{};
+    pa.mode = kModeMuxTree;
+    pa.ca = x;
+    pa.cb = nodes[k & 1];
+    pa.bits = msg_bits;
+    pa.group = int64_t{1} << (msg_bits - k);
+    pa.out_bits = out_bits;
+    pa.level = k - 1;
+    pa.B = 2 * V * out_bits * pa.group;
+    uint32_t* dst = k == msg_bits ? out : nodes[(k + 1) & 1];
+    if ((rc = mux_common(ek, pa, dst, base + L.ws_off, L.total - L.ws_off, stream))) return rc;
+  }
+  return TFHE_OK;
+}
+
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {
   if (dim < 1 || count < 0) return fail(TFHE_EINVAL, "need dim >= 1 and count >= 0");
   if (count == 0) return TFHE_OK;

@@ -60,17 +60,30 @@ struct Workspace {
 int64_t workspace_bytes(const tfhe_params& p, int64_t B);
 Workspace carve_workspace(const tfhe_params& p, void* ws, int64_t B);
 
-enum InputMode : int { kModeGate = 0, kModePlain = 1, kModeRelu = 2, kModeIRelu = 3 };
+enum InputMode : int {
+  kModeGate = 0,      // two-input gate on (ca[c], cb[c])
+  kModePlain = 1,     // ca[c] as is
+  kModeRelu = 2,      // forward ReLU gates over x = ca
+  kModeIRelu = 3,     // backward iReLU gates: sign of u = ca, error bits cb
+  kModeMux = 4,       // multiplexer halves: AND(ca, cb), AND(NOT ca, cc)
+  kModeMuxTree = 5,   // one level of a multiplexer tree (see prep_kernel)
+};
 
+// Inputs of the preparation kernel (gate combination and modulus switch).
+// In the multiplexer modes B counts the two halves of every multiplexer.
 struct PrepArgs {
   int mode;
   int gate;
-  const uint32_t* ca;  // gate: first operand; plain: the input; relu: x; irelu: u
-  const uint32_t* cb;  // gate: second operand; irelu: delta
+  const uint32_t* ca;  // gate: first operand; plain: the input; relu: x; irelu: u; mux: selectors
+  const uint32_t* cb;  // gate: second operand; irelu: delta; mux: if-true; mux tree: the level's children
   int64_t B;
-  int32_t bits;        // relu: bits of x; irelu: bits of delta
+  int32_t bits;        // relu: bits of x; irelu: bits of delta; mux tree: selector bits per value
   int64_t gate_begin;  // relu, irelu
   int32_t sign_bits;   // irelu: bits of u (its sign is bit sign_bits - 1)
+  const uint32_t* cc;  // mux: if-false
+  int64_t group;       // mux tree: nodes per (value, output bit) at this level
+  int32_t out_bits;    // mux tree: output bits per value
+  int32_t level;       // mux tree: selector bit of this level
 };
 
 int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws, void* stream);
@@ -81,6 +94,12 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
 int launch_relu_sign(const tfhe_eval_key* ek, uint32_t* y, int32_t bits, int64_t v_begin,
                      int64_t v_end, void* stream);
 int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);
+// ext[e] += ext[M + e] + (0, 1/8) for e < M (the multiplexer's OR of its halves)
+int launch_mux_combine(const tfhe_eval_key* ek, uint32_t* ext, int64_t M, void* stream);
+// first level of a multiplexer tree over constant leaves table[k]: node
+// (v, o, j) selects bit o of table[2j + x[v][0]]
+int launch_lut_leaf(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits, const uint32_t* table,
+                    int32_t out_bits, int64_t V, uint32_t* nodes, void* stream);
 int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
                           uint32_t* c, int64_t B, void* stream);
 

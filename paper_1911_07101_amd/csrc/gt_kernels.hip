@@ -270,40 +270,100 @@ __device__ __forceinline__ GateCoef gate_coef(int gate) {
   }
 }
 
-__global__ __launch_bounds__(256) void prep_kernel(int mode, int gate, const uint32_t* __restrict__ ca,
-                                                   const uint32_t* __restrict__ cb, int n, int N,
-                                                   int64_t B, int32_t bits, int32_t sign_bits,
-                                                   int64_t gate_begin, uint16_t* __restrict__ abar) {
+__global__ __launch_bounds__(256) void prep_kernel(PrepArgs a, int n, int N, uint16_t* __restrict__ abar) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const int64_t total = B * (n + 1);
+  const int64_t total = a.B * (n + 1);
   if (idx >= total) return;
   const int64_t c = idx / (n + 1);
   const int k = static_cast<int>(idx - c * (n + 1));
+  const int64_t row = n + 1;
   uint32_t x;
-  if (mode == kModePlain) {
-    x = ca[c * (n + 1) + k];
+  if (a.mode == kModePlain) {
+    x = a.ca[c * row + k];
   } else {
     const uint32_t* pa;
     const uint32_t* pb;
-    if (mode == kModeRelu) {
-      const int64_t g = gate_begin + c;
-      const int64_t v = g / (bits - 1), i = g - v * (bits - 1);
-      pa = ca + (v * bits + (bits - 1)) * (n + 1);  // sign bit
-      pb = ca + (v * bits + i) * (n + 1);
-    } else if (mode == kModeIRelu) {
-      const int64_t g = gate_begin + c;
-      const int64_t v = g / bits;
-      pa = ca + (v * sign_bits + (sign_bits - 1)) * (n + 1);  // sign bit of u
-      pb = cb + g * (n + 1);                                   // error bit g % bits of value v
+    int gate = a.gate;
+    if (a.mode == kModeRelu) {
+      const int64_t g = a.gate_begin + c;
+      const int64_t v = g / (a.bits - 1), i = g - v * (a.bits - 1);
+      pa = a.ca + (v * a.bits + (a.bits - 1)) * row;  // sign bit
+      pb = a.ca + (v * a.bits + i) * row;
+      gate = TFHE_ANDNY;
+    } else if (a.mode == kModeIRelu) {
+      const int64_t g = a.gate_begin + c;
+      const int64_t v = g / a.bits;
+      pa = a.ca + (v * a.sign_bits + (a.sign_bits - 1)) * row;  // sign bit of u
+      pb = a.cb + g * row;                                       // error bit g % bits of value v
+      gate = TFHE_ANDNY;
+    } else if (a.mode == kModeMux || a.mode == kModeMuxTree) {
+      // multiplexer e = c mod M: first half AND(selector, if-true), second
+      // half AND(NOT selector, if-false)
+      const int64_t M = a.B / 2;
+      const bool second = c >= M;
+      const int64_t e = second ? c - M : c;
+      if (a.mode == kModeMux) {
+        pa = a.ca + e * row;
+        pb = (second ? a.cc : a.cb) + e * row;
+      } else {
+        // node j of group (v, o) at this level: children 2j (selector bit 0)
+        // and 2j + 1 (selector bit 1) of the level below, selector bit
+        // `level` of value v
+        const int64_t grp = e / a.group, j = e - grp * a.group;
+        const int64_t v = grp / a.out_bits;
+        pa = a.ca + (v * a.bits + a.level) * row;
+        pb = a.cb + (grp * 2 * a.group + 2 * j + (second ? 0 : 1)) * row;
+      }
+      gate = second ? TFHE_ANDNY : TFHE_AND;
     } else {
-      pa = ca + c * (n + 1);
-      pb = cb + c * (n + 1);
+      pa = a.ca + c * row;
+      pb = a.cb + c * row;
     }
-    const GateCoef gc = gate_coef(mode == kModeGate ? gate : static_cast<int>(TFHE_ANDNY));
+    const GateCoef gc = gate_coef(gate);
     x = static_cast<uint32_t>(gc.wa) * pa[k] + static_cast<uint32_t>(gc.wb) * pb[k] +
         (k == n ? gc.konst : 0u);
   }
   abar[idx] = mod_switch(x, N);
+}
+
+// ext[e] += ext[M + e] + (0, 1/8): the OR of a multiplexer's two halves, of
+// which at most one is true (N + 1 words per sample)
+__global__ __launch_bounds__(256) void mux_combine_kernel(uint32_t* __restrict__ ext, int N, int64_t M) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t row = N + 1;
+  if (idx >= M * row) return;
+  const int k = static_cast<int>(idx % row);
+  ext[idx] += ext[M * row + idx] + (k == N ? kMu : 0u);
+}
+
+struct LutTable {
+  uint32_t s[64];
+};
+
+// First level of a multiplexer tree over constant leaves: node (v, o, j)
+// chooses between bit o of table[2j] (x[v][0] false) and of table[2j + 1]
+// (x[v][0] true), i.e. a constant, x[v][0] or NOT x[v][0]; no bootstrap
+__global__ __launch_bounds__(256) void lut_leaf_kernel(const uint32_t* __restrict__ x, int n, int32_t msg_bits,
+                                                       LutTable table, int32_t out_bits, int64_t V,
+                                                       uint32_t* __restrict__ nodes) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t row = n + 1;
+  const int64_t W = int64_t{1} << (msg_bits - 1);
+  if (idx >= V * out_bits * W * row) return;
+  const int64_t node = idx / row;
+  const int k = static_cast<int>(idx - node * row);
+  const int64_t j = node % W, grp = node / W;
+  const int o = static_cast<int>(grp % out_bits);
+  const int64_t v = grp / out_bits;
+  const uint32_t b0 = (table.s[2 * j] >> o) & 1u, b1 = (table.s[2 * j + 1] >> o) & 1u;
+  uint32_t w;
+  if (b0 == b1) {
+    w = k == n ? (b0 ? kMu : 0u - kMu) : 0u;
+  } else {
+    const uint32_t xs = x[(v * msg_bits) * row + k];
+    w = b1 ? xs : 0u - xs;
+  }
+  nodes[idx] = w;
 }
 
 // ------------------------------------------------------ blind rotation
@@ -874,8 +934,7 @@ int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws,
   const int64_t total = a.B * (ek->p.n + 1);
   const int64_t blocks = (total + 255) / 256;
   hipLaunchKernelGGL(prep_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), a.mode, a.gate, a.ca, a.cb, ek->p.n, ek->p.N,
-                     a.B, a.bits, a.sign_bits, a.gate_begin, ws.abar);
+                     static_cast<hipStream_t>(stream), a, ek->p.n, ek->p.N, ws.abar);
   return launch_status("prep_kernel");
 }
 
@@ -921,6 +980,26 @@ int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, vo
   hipLaunchKernelGGL(not_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), in, out, words);
   return launch_status("not_kernel");
+}
+
+int launch_mux_combine(const tfhe_eval_key* ek, uint32_t* ext, int64_t M, void* stream) {
+  const int64_t words = M * (ek->p.N + 1);
+  if (words == 0) return TFHE_OK;
+  hipLaunchKernelGGL(mux_combine_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), ext, ek->p.N, M);
+  return launch_status("mux_combine_kernel");
+}
+
+int launch_lut_leaf(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits, const uint32_t* table,
+                    int32_t out_bits, int64_t V, uint32_t* nodes, void* stream) {
+  if (msg_bits < 1 || msg_bits > 6) return fail(TFHE_EUNSUPPORTED, "table lookup over %d bits", msg_bits);
+  LutTable t{};
+  for (int k = 0; k < (1 << msg_bits); k++) t.s[k] = table[k];
+  const int64_t words = V * out_bits * (int64_t{1} << (msg_bits - 1)) * (ek->p.n + 1);
+  if (words == 0) return TFHE_OK;
+  hipLaunchKernelGGL(lut_leaf_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), x, ek->p.n, msg_bits, t, out_bits, V, nodes);
+  return launch_status("lut_leaf_kernel");
 }
 
 int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c,

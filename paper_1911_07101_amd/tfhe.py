@@ -67,6 +67,9 @@ _SIGNATURES = {
     "tfhe_keyswitch_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _vp]),
     "glyph_relu_batch": (ctypes.c_int, [_vp, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
     "glyph_irelu_batch": (ctypes.c_int, [_vp, _vp, _i32, _vp, _vp, _i64, _i32, _i64, _i64, _vp, _i64, _vp]),
+    "tfhe_mux_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
+    "glyph_mux_lut_batch": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i32, _vp, _i64, _vp, _i64, _vp]),
+    "glyph_mux_lut_workspace_bytes": (_i64, [_vp, _i64, _i32, _i32]),
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
@@ -322,6 +325,44 @@ def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate
     ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
     _check(lib().glyph_irelu_batch(ek.handle, _dptr(u), u_bits, _dptr(delta), _dptr(out), V, bits,
                                    gate_begin, gate_end, _dptr(ws), ws.numel(), _stream(stream)))
+    return out
+
+
+def tfhe_mux_batch(ek: EvalKey, c, a, b, out=None, workspace=None, stream=None):
+    """out[e] encrypts c[e] ? a[e] : b[e]; all [B][n+1] device."""
+    B = c.shape[0]
+    out = _empty((B, ek.params.n + 1), ek) if out is None else out
+    ws = alloc_workspace(ek, 2 * B) if workspace is None else workspace
+    _check(lib().tfhe_mux_batch(ek.handle, _dptr(c), _dptr(a), _dptr(b), _dptr(out), B, _dptr(ws),
+                                ws.numel(), _stream(stream)))
+    return out
+
+
+def glyph_mux_lut_workspace_bytes(ek: EvalKey, V: int, msg_bits: int, out_bits: int) -> int:
+    r = lib().glyph_mux_lut_workspace_bytes(ek.handle, V, msg_bits, out_bits)
+    if r < 0:
+        _check(int(r))
+    return int(r)
+
+
+def alloc_mux_lut_workspace(ek: EvalKey, V: int, msg_bits: int, out_bits: int):
+    import torch
+    return torch.empty(max(glyph_mux_lut_workspace_bytes(ek, V, msg_bits, out_bits), 1), dtype=torch.uint8,
+                       device=f"cuda:{ek.device}")
+
+
+def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspace=None, stream=None):
+    """Table lookup by a multiplexer tree: x [V][msg_bits][n+1] encrypted bits
+    (LSB first) select entries of the public table (2^msg_bits values below
+    2^out_bits); returns out [V][out_bits][n+1]."""
+    V, msg_bits = x.shape[0], x.shape[1]
+    t = _host_u32(table)
+    if t.size != 1 << msg_bits:
+        raise ValueError(f"table needs {1 << msg_bits} entries")
+    out = _empty((V, out_bits, ek.params.n + 1), ek) if out is None else out
+    ws = alloc_mux_lut_workspace(ek, V, msg_bits, out_bits) if workspace is None else workspace
+    _check(lib().glyph_mux_lut_batch(ek.handle, _dptr(x), msg_bits, _hptr(t), out_bits, _dptr(out), V,
+                                     _dptr(ws), ws.numel(), _stream(stream)))
     return out
 
 

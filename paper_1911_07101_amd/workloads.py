@@ -40,6 +40,11 @@ CONFIGS = {
     # forward 8-bit pre-activations
     "mlp_irelu": dict(params=_TFHE_1024, kind="irelu", values=60 * 128, bits=8,
                       key_seed=0x19110715, input_seed=0x5EED0006, sample=64),
+    # the paper's 3-bit softmax exponentiation unit as a multiplexer tree on
+    # bit-wise encrypted inputs (128-bit parameters), over the same messages
+    # and table as the LUT bootstrap below
+    "softmax_mux3": dict(params=_TFHE_1024, kind="mux_lut", values=8192, msg_bits=3, out_bits=3,
+                         key_seed=0x19110716, input_seed=0x5EED0005, sample=8),
     # programmable (table-lookup) bootstrap on 3-bit messages, N = 2048
     "lut3_n2048": dict(params=dict(n=750, N=2048, l=2, bg_bit=10, ks_t=8, ks_basebit=2,
                                    alpha_lwe=2.0 ** -17, alpha_bk=2.0 ** -45,

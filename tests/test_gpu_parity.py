@@ -254,6 +254,39 @@ def test_irelu_window_writes_only_its_gates(torch):
     assert np.array_equal(got[7:23], oracle.irelu_gates(ok, cu, 3, cd, bits, np.arange(7, 23)))
 
 
+def test_mux_toy(torch):
+    """Multiplexers on random encrypted bits: bit-exact with the oracle and
+    decrypting to c ? a : b."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    B = 37
+    rng = np.random.default_rng(23)
+    bits = rng.integers(0, 2, (3, B))
+    cts = [tfhe.tfhe_encrypt_torus(sk, 40 + k, tfhe.encode_bits(bits[k])) for k in range(3)]
+    say(f"mux toy B={B}")
+    got = tfhe.to_host(tfhe.tfhe_mux_batch(ek, *[tfhe.to_device(c) for c in cts]))
+    assert np.array_equal(got, oracle.mux(ok, *cts))
+    assert np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, got)), np.where(bits[0] == 1, bits[1], bits[2]))
+
+
+@pytest.mark.parametrize("msg_bits,out_bits", [(1, 3), (2, 2), (3, 3), (4, 2)])
+def test_mux_lut_toy(torch, msg_bits, out_bits):
+    """Multiplexer-tree table lookup over every input, repeated into a ragged
+    batch: bit-exact with the oracle and decrypting to the table entry."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    rng = np.random.default_rng(100 + msg_bits)
+    table = rng.integers(0, 1 << out_bits, 1 << msg_bits).astype(np.uint32)
+    xs = np.resize(np.arange(1 << msg_bits), 19)
+    ct = tfhe.tfhe_encrypt_torus(sk, 50 + msg_bits, tfhe.encode_bits(wl.to_bits(xs, msg_bits).ravel()))
+    ct = ct.reshape(len(xs), msg_bits, p["n"] + 1)
+    say(f"mux lut toy msg_bits={msg_bits} out_bits={out_bits} V={len(xs)}")
+    got = tfhe.to_host(tfhe.glyph_mux_lut_batch(ek, tfhe.to_device(ct), table, out_bits))
+    assert np.array_equal(got, oracle.mux_lut(ok, ct, msg_bits, table, out_bits))
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(len(xs), out_bits)
+    assert np.array_equal((dec.astype(np.int64) << np.arange(out_bits)).sum(axis=1), table[xs])
+
+
 # ---------------------------------------------------- full-size workloads
 
 def test_tfhe128_nand_4096(torch):
@@ -324,6 +357,32 @@ def test_mlp_irelu_7680(torch):
     gates = wl.sample_indices(cfg["input_seed"], total, cfg["sample"])
     ref = oracle.irelu_gates(ok, cu, 8, cd, 8, gates)
     assert np.array_equal(got.reshape(-1, p["n"] + 1)[gates], ref)
+
+
+def test_softmax_mux3_8192(torch):
+    """The 3-bit softmax exponentiation unit by multiplexer tree on 8192
+    bit-wise encrypted values (128-bit parameters, the LUT workload's
+    messages and table): every output decrypts to its table entry, and a
+    sample matches the oracle bit for bit."""
+    cfg = wl.CONFIGS["softmax_mux3"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)  # same parameter set, shared keys
+    V, mb, ob = cfg["values"], cfg["msg_bits"], cfg["out_bits"]
+    m = wl.messages(cfg["input_seed"], V, mb)
+    table = wl.lut(cfg["input_seed"], mb)
+    ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(wl.to_bits(m, mb).ravel()))
+    ct = ct.reshape(V, mb, p["n"] + 1)
+    say(f"softmax mux tree n=630 V={V}")
+    t0 = time.time()
+    got = tfhe.to_host(tfhe.glyph_mux_lut_batch(ek, tfhe.to_device(ct), table, ob))
+    say(f"  gpu {time.time() - t0:.2f}s")
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(V, ob)
+    assert np.array_equal((dec.astype(np.int64) << np.arange(ob)).sum(axis=1), table[m])
+    idx = wl.sample_indices(cfg["input_seed"], V, cfg["sample"])
+    t0 = time.time()
+    ref = oracle.mux_lut(ok, ct[idx], mb, table, ob)
+    say(f"  oracle sample of {len(idx)} values in {time.time() - t0:.1f}s")
+    assert np.array_equal(got[idx], ref)
 
 
 def test_conv_relu_streamed(torch):

@@ -363,6 +363,34 @@ def test_irelu_all_4bit_pairs():
     assert np.array_equal(oracle.irelu_gates(keys, u, 4, d, 4, ids), y.reshape(-1, p["n"] + 1)[ids])
 
 
+def test_mux_truth_table():
+    """The multiplexer decrypts to c ? a : b for every input combination."""
+    p = TOY
+    keys = oracle.Keys(p, 1001)
+    bits = np.array([(c, a, b) for c in (0, 1) for a in (0, 1) for b in (0, 1)] * 2)
+    enc = lambda col, seed: oracle.encrypt(p["n"], keys.s, seed, p["alpha_lwe"],
+                                           np.where(bits[:, col] == 1, MU, M32 - MU))
+    out = oracle.mux(keys, enc(0, 81), enc(1, 82), enc(2, 83))
+    assert np.array_equal(decrypt_bits(keys.s, out), np.where(bits[:, 0] == 1, bits[:, 1], bits[:, 2]))
+
+
+@pytest.mark.parametrize("msg_bits,out_bits", [(1, 2), (2, 3), (3, 3)])
+def test_mux_lut_all_inputs(msg_bits, out_bits):
+    """The multiplexer tree returns the bits of table[x] for every input x
+    (Section 3.1's 3-bit softmax unit is msg_bits = out_bits = 3)."""
+    from paper_1911_07101_amd import workloads as wl
+    p = TOY
+    keys = oracle.Keys(p, 1002 + msg_bits)
+    rng = np.random.default_rng(msg_bits)
+    table = rng.integers(0, 1 << out_bits, 1 << msg_bits)
+    xs = np.arange(1 << msg_bits)
+    x = oracle.encrypt(p["n"], keys.s, 84, p["alpha_lwe"],
+                       np.where(wl.to_bits(xs, msg_bits).ravel() == 1, MU, M32 - MU))
+    out = oracle.mux_lut(keys, x.reshape(len(xs), msg_bits, p["n"] + 1), msg_bits, table, out_bits)
+    got = decrypt_bits(keys.s, out.reshape(-1, p["n"] + 1)).reshape(len(xs), out_bits)
+    assert np.array_equal((got << np.arange(out_bits)).sum(axis=1), table[xs])
+
+
 def test_lut_bootstrap_all_messages():
     p = dict(TOY, n=64, N=512)
     keys = oracle.Keys(p, 515)
