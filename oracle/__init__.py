@@ -4,7 +4,9 @@ The oracle is a plain, slow CPU implementation of TFHE gate bootstrapping
 (modulus switch, blind rotation with schoolbook negacyclic products, sample
 extraction, key switching), the Glyph forward ReLU and backward iReLU units,
 the homomorphic multiplexer and the softmax's multiplexer-tree table lookup,
-and the look-up-table bootstrap.  Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
+the look-up-table bootstrap, and the TFHE steps of the cryptosystem switch
+(packing key switching, SampleExtract of any coefficient, bootstrapping onto
+arbitrary torus values).  Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s
 ``cpu_baseline`` leg may import this package; the GPU library never does, and
 the two share no code.
 """
@@ -91,6 +93,11 @@ def _load():
                                      _u32p]),
         "oracle_not": (None, [ctypes.c_int32, _u32p, _u32p, ctypes.c_int64]),
         "oracle_threads": (ctypes.c_int, []),
+        "oracle_pks_words": (ctypes.c_int64, [P]),
+        "oracle_packing_keygen": (None, [P, ctypes.c_uint64, _u32p, _u32p, _u32p]),
+        "oracle_pack_keyswitch": (None, [P, _u32p, _u32p, ctypes.c_int32, _u32p]),
+        "oracle_sample_extract_at": (None, [ctypes.c_int32, _u32p, ctypes.c_int32, _u32p]),
+        "oracle_torus_testvec": (None, [ctypes.c_int32, ctypes.c_int32, _u32p, _u32p]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -183,6 +190,15 @@ class Keys:
     def ksk_view(self):
         p = self.p
         return self.ksk.reshape(p.N, p.ks_t, (1 << p.ks_basebit) - 1, p.n + 1)
+
+    def packing_key(self):
+        """Packing key of the functional key switching (computed on first use)."""
+        if getattr(self, "pks", None) is None:
+            p = self.p
+            lib = _load()
+            self.pks = np.zeros(lib.oracle_pks_words(ctypes.byref(p)), np.uint32)
+            lib.oracle_packing_keygen(ctypes.byref(p), self.seed, _u32(self.s), _u32(self.S), _u32(self.pks))
+        return self.pks
 
 
 def encrypt(dim, key, seed, alpha, mu, first_index=0):
@@ -387,6 +403,32 @@ def mux_lut(keys: Keys, x, msg_bits, table, out_bits):
             new[v][o].append(r)
         nodes = new
     return np.stack([np.stack([nodes[v][o][0] for o in range(out_bits)]) for v in range(V)])
+
+
+def pack_keyswitch(keys: Keys, lwe):
+    """Functional key switching of Z LWE samples into one TRLWE sample whose
+    phase is sum_z phase_z X^z (Section 3.2, step 2); returns [2][N]."""
+    p = keys.p
+    lwe = np.ascontiguousarray(lwe, dtype=np.uint32).reshape(-1, p.n + 1)
+    out = np.zeros(2 * p.N, np.uint32)
+    _load().oracle_pack_keyswitch(ctypes.byref(p), _u32(keys.packing_key()), _u32(lwe), len(lwe), _u32(out))
+    return out.reshape(2, p.N)
+
+
+def sample_extract_at(acc, idx):
+    """LWE sample of coefficient idx of the TRLWE sample acc ([2][N])."""
+    acc = np.ascontiguousarray(acc, dtype=np.uint32).ravel()
+    N = len(acc) // 2
+    out = np.zeros(N + 1, np.uint32)
+    _load().oracle_sample_extract_at(N, _u32(acc), idx, _u32(out))
+    return out
+
+
+def torus_testvec(N, msg_bits, values):
+    values = np.ascontiguousarray(values, dtype=np.uint32)
+    tv = np.zeros(N, np.uint32)
+    _load().oracle_torus_testvec(N, msg_bits, _u32(values), _u32(tv))
+    return tv
 
 
 def not_gate(ct):

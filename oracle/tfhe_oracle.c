@@ -414,3 +414,92 @@ int oracle_threads(void) {
   return 1;
 #endif
 }
+
+/* ------------------------------------------------------------------------
+ * TFHE side of the cryptosystem switch (Section 3.2: step 2, functional key
+ * switching from T^N to T_N[X]; step 3, SampleExtract of K coefficients;
+ * step 4, functional bootstrapping onto multiples of p^-r)
+ * ---------------------------------------------------------------------- */
+
+int64_t oracle_pks_words(const oracle_params* p) {
+  return (int64_t)p->n * p->ks_t * ((1 << p->ks_basebit) - 1) * 2 * p->N;
+}
+
+/* Packing key: entry u = (i, j, v), v in [1, base), is a TRLWE sample (A, B)
+ * under S of the constant polynomial v * s_i * 2^(32 - (j+1)*basebit):
+ * A uniform, B = A * S + e + message in coefficient 0, e a rounded Gaussian
+ * of deviation alpha_bk per coefficient. */
+void oracle_packing_keygen(const oracle_params* p, uint64_t seed, const uint32_t* s,
+                           const uint32_t* S, uint32_t* pks) {
+  const int32_t n = p->n, N = p->N, t = p->ks_t, bb = p->ks_basebit, vals = (1 << bb) - 1;
+#pragma omp parallel for schedule(dynamic)
+  for (int64_t u = 0; u < (int64_t)n * t * vals; u++) {
+    const int32_t i = (int32_t)(u / ((int64_t)t * vals));
+    const int32_t j = (int32_t)((u / vals) % t);
+    const uint32_t v = (uint32_t)(u % vals) + 1u;
+    uint32_t* A = pks + u * 2 * N;
+    uint32_t* B = A + N;
+    const uint64_t base_index = (uint64_t)u * (uint64_t)N;
+    for (int32_t m = 0; m < N; m++) A[m] = torus_word(seed, ORACLE_TAG_PKS_MASK, base_index + (uint64_t)m);
+    oracle_negacyclic_mul(N, A, S, B);
+    for (int32_t m = 0; m < N; m++)
+      B[m] += oracle_noise(seed, ORACLE_TAG_PKS_NOISE, base_index + (uint64_t)m, p->alpha_bk);
+    B[0] += v * s[i] * (1u << (32 - (j + 1) * bb));
+  }
+}
+
+/* Functional key switching with the packing morphism (mu_0..mu_{Z-1}) ->
+ * sum_z mu_z X^z: Z LWE samples (dimension n, key s) become one TRLWE
+ * sample (A, B) under S whose phase is sum_z phase_z X^z, plus key noise
+ * and the rounding of each a_{z,i} to t*basebit bits.  Start from
+ * (0, sum_z b_z X^z) and, for every sample z, coefficient i and non-zero
+ * digit v_{z,i,j} of the rounded a_{z,i} (most significant first),
+ * subtract X^z times the key entry (i, j, v). */
+void oracle_pack_keyswitch(const oracle_params* p, const uint32_t* pks, const uint32_t* lwe,
+                           int32_t Z, uint32_t* out) {
+  const int32_t n = p->n, N = p->N, t = p->ks_t, bb = p->ks_basebit, vals = (1 << bb) - 1;
+  const int32_t prec = t * bb;
+  const uint32_t round = prec < 32 ? (1u << (31 - prec)) : 0u;
+  uint32_t* A = out;
+  uint32_t* B = out + N;
+  uint32_t* rot = (uint32_t*)malloc(sizeof(uint32_t) * 2 * (size_t)N);
+  for (int32_t k = 0; k < 2 * N; k++) out[k] = 0;
+  for (int32_t z = 0; z < Z; z++) {
+    const uint32_t* c = lwe + (int64_t)z * (n + 1);
+    B[z] += c[n];
+    for (int32_t i = 0; i < n; i++) {
+      const uint32_t r = prec == 32 ? c[i] : (c[i] + round) >> (32 - prec);
+      for (int32_t j = 0; j < t; j++) {
+        const uint32_t v = (r >> ((t - 1 - j) * bb)) & (uint32_t)vals;
+        if (v == 0) continue;
+        const uint32_t* e = pks + (((int64_t)i * t + j) * vals + (v - 1)) * 2 * N;
+        oracle_rotate(N, e, (uint32_t)z, rot);
+        oracle_rotate(N, e + N, (uint32_t)z, rot + N);
+        for (int32_t k = 0; k < N; k++) {
+          A[k] -= rot[k];
+          B[k] -= rot[N + k];
+        }
+      }
+    }
+  }
+  free(rot);
+}
+
+/* SampleExtract of coefficient idx of (A, B): the LWE sample under the key
+ * (S_0 .. S_{N-1}) with a'_j = A_{idx-j} for j <= idx, -A_{N+idx-j} for
+ * j > idx, and b' = B_idx (coefficient idx of B - A*S is b' - <a', S>) */
+void oracle_sample_extract_at(int32_t N, const uint32_t* acc, int32_t idx, uint32_t* out) {
+  for (int32_t j = 0; j < N; j++) out[j] = j <= idx ? acc[idx - j] : 0u - acc[N + idx - j];
+  out[N] = acc[N + idx];
+}
+
+/* Test vector of a programmable bootstrap onto arbitrary torus values
+ * (step 4 maps messages onto multiples of p^-r): as oracle_lut_testvec, with
+ * values[m] (torus words) in place of lut[m] * 2^(31 - msg_bits). */
+void oracle_torus_testvec(int32_t N, int32_t msg_bits, const uint32_t* values, uint32_t* tv) {
+  const int64_t M = 1ll << msg_bits;
+  for (int32_t j = 0; j < N; j++) {
+    int64_t idx = (((int64_t)j + (int64_t)N / (2 * M)) * M) / N;
+    tv[j] = idx < M ? values[idx] : 0u - values[0];
+  }
+}

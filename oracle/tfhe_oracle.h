@@ -49,7 +49,8 @@ enum {
 enum {
   ORACLE_TAG_LWE_KEY = 1, ORACLE_TAG_RLWE_KEY = 2, ORACLE_TAG_BK_MASK = 3,
   ORACLE_TAG_BK_NOISE = 4, ORACLE_TAG_KSK_MASK = 5, ORACLE_TAG_KSK_NOISE = 6,
-  ORACLE_TAG_ENC_MASK = 7, ORACLE_TAG_ENC_NOISE = 8
+  ORACLE_TAG_ENC_MASK = 7, ORACLE_TAG_ENC_NOISE = 8, ORACLE_TAG_PKS_MASK = 9,
+  ORACLE_TAG_PKS_NOISE = 10
 };
 
 /* ---- randomness ------------------------------------------------------- */
@@ -99,6 +100,15 @@ void oracle_relu_gates(const oracle_params* p, const uint32_t* bk, const uint32_
                        int64_t count, uint32_t* out);
 void oracle_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count);
 int oracle_threads(void);
+
+/* ---- TFHE side of the cryptosystem switch (Section 3.2) ---------------- */
+int64_t oracle_pks_words(const oracle_params* p);  /* n * t * (base-1) * 2 * N */
+void oracle_packing_keygen(const oracle_params* p, uint64_t seed, const uint32_t* s,
+                           const uint32_t* S, uint32_t* pks);
+void oracle_pack_keyswitch(const oracle_params* p, const uint32_t* pks, const uint32_t* lwe,
+                           int32_t Z, uint32_t* out);
+void oracle_sample_extract_at(int32_t N, const uint32_t* acc, int32_t idx, uint32_t* out);
+void oracle_torus_testvec(int32_t N, int32_t msg_bits, const uint32_t* values, uint32_t* tv);
 
 #ifdef __cplusplus
 }

@@ -437,3 +437,99 @@ def test_gate_noise_matches_variance_estimate():
     sigma = math.sqrt(var_br + var_ks)
     assert 0.6 < err.std() / sigma < 1.5
     assert np.all(np.abs(err) < 0.125)
+
+
+# ------------------------------------- TFHE side of the switch (Section 3.2)
+
+def trlwe_phase(S, acc):
+    """B - A*S with the product by numpy.convolve (independent of the oracle)."""
+    A, B = acc[0], acc[1]
+    return ((B.astype(np.int64) - np_negacyclic(A, S).astype(np.int64)) % M32).astype(np.uint32)
+
+
+def test_sample_extract_at_every_coefficient():
+    """The extracted sample of coefficient i decrypts, under S, to
+    coefficient i of the TRLWE phase; coefficient 0 agrees with the
+    gate bootstrap's SampleExtract."""
+    N = 64
+    rng = np.random.default_rng(3)
+    S = rng.integers(0, 2, N).astype(np.uint32)
+    acc = rng.integers(0, M32, (2, N), dtype=np.uint64).astype(np.uint32)
+    ph = trlwe_phase(S, acc)
+    for i in range(N):
+        e = oracle.sample_extract_at(acc, i)
+        assert oracle.phase(S, e[None])[0] == ph[i], i
+    assert np.array_equal(oracle.sample_extract_at(acc, 0), oracle.sample_extract(acc))
+
+
+def test_packing_key_entries_decrypt_to_their_messages():
+    """Every packing-key entry (i, j, v) is a TRLWE sample under S of the
+    constant v * s_i * 2^(32-(j+1)*basebit), up to the key noise."""
+    p = dict(TOY, n=8, N=64)
+    keys = oracle.Keys(p, 4242)
+    t, bb = p["ks_t"], p["ks_basebit"]
+    pks = keys.packing_key().reshape(p["n"], t, (1 << bb) - 1, 2, p["N"])
+    for i in range(p["n"]):
+        for j in range(t):
+            for v in range(1, 1 << bb):
+                ph = s32(trlwe_phase(keys.S, pks[i, j, v - 1]))
+                want = np.zeros(p["N"], np.int64)
+                want[0] = s32(v * int(keys.s[i]) << (32 - (j + 1) * bb))
+                assert np.all(np.abs(s32(ph - want)) < 2 ** 32 * 2.0 ** -20), (i, j, v)
+
+
+def test_pack_keyswitch_trivial_inputs_exact():
+    """Samples with a = 0 pack into exactly (0, sum_z b_z X^z)."""
+    p = dict(TOY, n=8, N=64)
+    keys = oracle.Keys(p, 4243)
+    Z = 40
+    lwe = np.zeros((Z, p["n"] + 1), np.uint32)
+    lwe[:, -1] = np.random.default_rng(4).integers(0, M32, Z, dtype=np.uint64).astype(np.uint32)
+    acc = oracle.pack_keyswitch(keys, lwe)
+    assert np.all(acc[0] == 0)
+    assert np.array_equal(acc[1][:Z], lwe[:, -1]) and np.all(acc[1][Z:] == 0)
+
+
+def test_pack_keyswitch_packs_the_phases():
+    """Z fresh LWE samples of messages m_z / 64 pack into a TRLWE whose phase
+    coefficient z is m_z / 64 up to rounding and noise (coefficients >= Z are
+    near 0), checked with an independent product; extracting coefficient z
+    again gives an LWE sample of m_z / 64."""
+    p = TOY
+    keys = oracle.Keys(p, 4244)
+    Z = 100
+    m = np.random.default_rng(5).integers(0, 64, Z).astype(np.uint32)
+    lwe = oracle.encrypt(p["n"], keys.s, 91, p["alpha_lwe"], m << 26)
+    acc = oracle.pack_keyswitch(keys, lwe)
+    ph = trlwe_phase(keys.S, acc).astype(np.int64)
+    assert np.array_equal(((ph + (1 << 25)) >> 26) % 64, np.concatenate([m, np.zeros(p["N"] - Z, np.uint32)]))
+    err = s32(ph - np.concatenate([m.astype(np.int64) << 26, np.zeros(p["N"] - Z, np.int64)]))
+    assert np.max(np.abs(err)) < 2 ** 32 * 2.0 ** -10  # rounding to 16 bits over n = 64 terms, plus noise
+    for z in (0, 17, Z - 1):
+        e = oracle.sample_extract_at(acc, z)
+        assert ((int(oracle.phase(keys.S, e[None])[0]) + (1 << 25)) >> 26) % 64 == m[z]
+
+
+def test_torus_testvec_generalises_lut_testvec():
+    N = 256
+    lut = np.random.default_rng(6).integers(0, 8, 8).astype(np.uint32)
+    assert np.array_equal(oracle.torus_testvec(N, 3, lut << 28), oracle.lut_testvec(N, 3, lut))
+
+
+def test_functional_bootstrap_onto_multiples_of_inverse_modulus():
+    """Bootstrapping with a test vector of multiples of 1/q (q = p^r = 257)
+    maps a 3-bit message m to f(m)/q (Section 3.2, step 4); the result is
+    taken before key switching (the next step switches into BGV), with a
+    low-noise bootstrapping key as in the N = 2048 LUT parameters: its phase
+    under S times q rounds to f(m)."""
+    p = dict(TOY, N=512, alpha_bk=2.0 ** -45)
+    keys = oracle.Keys(p, 4245)
+    q = 257
+    f = np.random.default_rng(7).integers(0, q, 8)
+    values = np.array([(int(v) * (1 << 32) + q // 2) // q for v in f], dtype=np.uint64).astype(np.uint32)
+    tv = oracle.torus_testvec(p["N"], 3, values)
+    m = np.arange(8, dtype=np.uint32).repeat(2)
+    ct = oracle.encrypt(p["n"], keys.s, 92, p["alpha_lwe"], m << 28)
+    out = oracle.bootstrap_no_ks(keys, ct, tv)
+    ph = oracle.phase(keys.S, out).astype(np.int64)
+    assert np.array_equal(((ph * q + (1 << 31)) >> 32) % q, f[m])
