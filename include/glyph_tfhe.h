@@ -234,6 +234,45 @@ int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_
 int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_t msg_bits,
                                       int32_t out_bits);
 
+/* ---- TFHE side of the cryptosystem switch (Section 3.2) ----------------
+ * From BGV to TFHE, step 2 packs LWE samples into a TRLWE sample by
+ * functional key switching and step 3 extracts LWE samples of its
+ * coefficients; from TFHE to BGV, step 4 bootstraps onto multiples of
+ * p^-r (a programmable bootstrap with tfhe_torus_testvec).  The BGV side of
+ * either direction is not part of this library. */
+
+/* Client side: build the packing key from the secret key (entry (i, j, v),
+ * v in [1, 2^ks_basebit), is a TRLWE sample under S of the constant
+ * polynomial v * s_i * 2^(32 - (j+1)*ks_basebit), noise alpha_bk) and add it
+ * to the eval key on its device.  n * ks_t * (2^ks_basebit - 1) * 2N words
+ * (124 MB at n = 630, N = 1024); a second call is a no-op. */
+int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek);
+
+/* Client side: copy the packing key (built on first use) to host memory,
+ * [n][ks_t][2^ks_basebit - 1][2][N] words. */
+int tfhe_export_packing_key(tfhe_secret_key* sk, uint32_t* pks);
+
+/* Step 2: functional key switching with the packing morphism.  lwe:
+ * [B][Z][n+1] device, Z <= N samples per output under s; out: [B][2][N]
+ * device, TRLWE samples (A, B) under S whose phase is sum_z phase_z X^z up to
+ * the rounding of each a_{z,i} to ks_t * ks_basebit bits and the key noise.
+ * Needs the packing key (tfhe_packing_key_upload), ks_t * ks_basebit <= 16
+ * and ks_basebit <= 2.  out must not alias lwe. */
+int tfhe_pack_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out,
+                              int64_t B, void* stream);
+
+/* Step 3: SampleExtract of coefficients 0 .. K-1 of B TRLWE samples
+ * ([B][2][N] device) into [B][K][N+1] device LWE samples under S: sample i
+ * is (a'_0 .. a'_{N-1}, B_i) with a'_j = A_{i-j} for j <= i and -A_{N+i-j}
+ * for j > i; its phase is coefficient i of B - A*S. */
+int tfhe_sample_extract_batch(int32_t N, const uint32_t* trlwe, int64_t B, int32_t K, uint32_t* out,
+                              void* stream);
+
+/* Host: test polynomial of a programmable bootstrap onto arbitrary torus
+ * values (step 4 uses multiples of p^-r): as tfhe_lut_testvec with
+ * values[m] (2^msg_bits torus words) in place of lut[m] * 2^(31-msg_bits). */
+int tfhe_torus_testvec(int32_t N, int32_t msg_bits, const uint32_t* values, uint32_t* tv);
+
 /* NOT without bootstrapping (Section 3.1): out = -in word by word.
  * in, out: [count][dim+1] device. */
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);

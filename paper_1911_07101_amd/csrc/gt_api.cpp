@@ -196,6 +196,8 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   ek->bk_fft = nullptr;
   ek->tw = nullptr;
   ek->ksk = nullptr;
+  ek->pks = nullptr;
+  ek->pks_bytes = 0;
   // [n][2l][2 * parts][N/2] complex doubles
   ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
   ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
@@ -269,6 +271,7 @@ void tfhe_eval_key_free(tfhe_eval_key* ek) {
   if (ek->bk_fft) (void)hipFree(ek->bk_fft);
   if (ek->tw) (void)hipFree(ek->tw);
   if (ek->ksk) (void)hipFree(ek->ksk);
+  if (ek->pks) (void)hipFree(ek->pks);
   delete ek;
 }
 
@@ -284,6 +287,44 @@ int tfhe_export_keys(const tfhe_secret_key* sk, uint32_t* s, uint32_t* S, uint32
   if (S) std::memcpy(S, sk->S.data(), sk->S.size() * 4);
   if (bk) std::memcpy(bk, sk->bk.data(), sk->bk.size() * 4);
   if (ksk) std::memcpy(ksk, sk->ksk.data(), sk->ksk.size() * 4);
+  return TFHE_OK;
+}
+
+int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek) {
+  if (!sk || !ek) return fail(TFHE_EINVAL, "NULL argument to tfhe_packing_key_upload");
+  const tfhe_params &a = sk->p, &b = ek->p;
+  if (a.n != b.n || a.N != b.N || a.l != b.l || a.bg_bit != b.bg_bit || a.ks_t != b.ks_t ||
+      a.ks_basebit != b.ks_basebit || a.alpha_bk != b.alpha_bk)
+    return fail(TFHE_EINVAL, "secret key and eval key have different parameters");
+  if (ek->pks) return TFHE_OK;
+  try {
+    if (sk->pks.empty()) packing_keygen_host(*sk);
+  } catch (const std::bad_alloc&) {
+    return fail(TFHE_ENOMEM, "host allocation failed for the packing key");
+  }
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  const int64_t bytes = static_cast<int64_t>(sk->pks.size()) * 4;
+  uint32_t* d = nullptr;
+  hipError_t e;
+  if ((e = hipMalloc(&d, bytes)) != hipSuccess) return fail(TFHE_ENOMEM, "hipMalloc(pks): %s", hipGetErrorString(e));
+  if ((e = hipMemcpy(d, sk->pks.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess) {
+    (void)hipFree(d);
+    return hip_fail(e, "copy pks");
+  }
+  ek->pks = d;
+  ek->pks_bytes = bytes;
+  return TFHE_OK;
+}
+
+int tfhe_export_packing_key(tfhe_secret_key* sk, uint32_t* pks) {
+  if (!sk || !pks) return fail(TFHE_EINVAL, "NULL argument to tfhe_export_packing_key");
+  try {
+    if (sk->pks.empty()) packing_keygen_host(*sk);
+  } catch (const std::bad_alloc&) {
+    return fail(TFHE_ENOMEM, "host allocation failed for the packing key");
+  }
+  std::memcpy(pks, sk->pks.data(), sk->pks.size() * 4);
   return TFHE_OK;
 }
 
@@ -306,6 +347,19 @@ int tfhe_decrypt_phase(const tfhe_secret_key* sk, int key_kind, const uint32_t* 
   if (!ct || !phase) return fail(TFHE_EINVAL, "NULL buffer");
   PhaseCtx ctx{key_kind == 0 ? &sk->s : &sk->S, ct, phase};
   parallel_for(count, 4096, phase_rows, &ctx);
+  return TFHE_OK;
+}
+
+int tfhe_torus_testvec(int32_t N, int32_t msg_bits, const uint32_t* values, uint32_t* tv) {
+  if (!values || !tv) return fail(TFHE_EINVAL, "NULL buffer");
+  if (msg_bits < 1 || msg_bits > 30 || N < (2 << msg_bits) || (N & (N - 1)) != 0)
+    return fail(TFHE_EINVAL, "need N a power of two with N >= 2^(msg_bits+1), 1 <= msg_bits <= 30");
+  const int64_t M = int64_t{1} << msg_bits;
+  const int64_t box = N / M;  // coefficients per table entry
+  for (int32_t j = 0; j < N; j++) {
+    const int64_t idx = (j + box / 2) / box;
+    tv[j] = idx < M ? values[idx] : 0u - values[0];
+  }
   return TFHE_OK;
 }
 
@@ -558,6 +612,29 @@ int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_
     if ((rc = mux_common(ek, pa, dst, base + L.ws_off, L.total - L.ws_off, stream))) return rc;
   }
   return TFHE_OK;
+}
+
+int tfhe_pack_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
+                              void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (!ek->pks) return fail(TFHE_EINVAL, "the eval key has no packing key (call tfhe_packing_key_upload)");
+  if (B < 0 || Z < 1 || Z > ek->p.N) return fail(TFHE_EINVAL, "need B >= 0 and 1 <= Z <= N");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(lwe, "lwe")) || (rc = check_u32(out, "out"))) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  return launch_pack_keyswitch(ek, lwe, Z, out, B, stream);
+}
+
+int tfhe_sample_extract_batch(int32_t N, const uint32_t* trlwe, int64_t B, int32_t K, uint32_t* out,
+                              void* stream) {
+  if (N < 2 || N > 4096 || (N & (N - 1))) return fail(TFHE_EINVAL, "N must be a power of two in [2, 4096]");
+  if (B < 0 || K < 1 || K > N) return fail(TFHE_EINVAL, "need B >= 0 and 1 <= K <= N");
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(trlwe, "trlwe")) || (rc = check_u32(out, "out"))) return rc;
+  return launch_sample_extract(N, trlwe, B, K, out, stream);
 }
 
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {

@@ -132,7 +132,36 @@ void ksk_rows(int64_t begin, int64_t end, void* vctx) {
   }
 }
 
+// packing key entry u = (i, j, v): TRLWE sample under S of the constant
+// polynomial v * s_i * 2^(32 - (j+1)*basebit)
+void pks_rows(int64_t begin, int64_t end, void* vctx) {
+  tfhe_secret_key& sk = *static_cast<KeygenCtx*>(vctx)->sk;
+  const tfhe_params& p = sk.p;
+  const int N = p.N, t = p.ks_t, bb = p.ks_basebit, vals = (1 << bb) - 1;
+  std::vector<uint32_t> body(N);
+  for (int64_t u = begin; u < end; u++) {
+    const int i = static_cast<int>(u / (static_cast<int64_t>(t) * vals));
+    const int j = static_cast<int>((u / vals) % t);
+    const uint32_t v = static_cast<uint32_t>(u % vals) + 1u;
+    uint32_t* A = sk.pks.data() + u * 2 * N;
+    uint32_t* Bp = A + N;
+    const uint64_t base = static_cast<uint64_t>(u) * static_cast<uint64_t>(N);
+    for (int m = 0; m < N; m++) A[m] = rand_torus(sk.seed, kTagPksMask, base + m);
+    trlwe_body(N, A, sk.S.data(), body.data());
+    for (int m = 0; m < N; m++) Bp[m] = body[m] + rand_noise(sk.seed, kTagPksNoise, base + m, p.alpha_bk);
+    Bp[0] += v * sk.s[i] * (1u << (32 - (j + 1) * bb));
+  }
+}
+
 }  // namespace
+
+void packing_keygen_host(tfhe_secret_key& sk) {
+  const tfhe_params& p = sk.p;
+  const int64_t entries = static_cast<int64_t>(p.n) * p.ks_t * ((1 << p.ks_basebit) - 1);
+  sk.pks.assign(static_cast<size_t>(entries) * 2 * p.N, 0u);
+  KeygenCtx ctx{&sk};
+  parallel_for(entries, 8, pks_rows, &ctx);
+}
 
 void keygen_host(tfhe_secret_key& sk) {
   const tfhe_params& p = sk.p;

@@ -13,6 +13,7 @@ struct tfhe_secret_key {
   std::vector<uint32_t> S;    // [N] 0/1
   std::vector<uint32_t> bk;   // [n][2l][2][N] coefficient domain
   std::vector<uint32_t> ksk;  // [N][t][base-1][n+1]
+  std::vector<uint32_t> pks;  // packing key [n][t][base-1][2][N], built on request
 };
 
 struct tfhe_eval_key {
@@ -22,8 +23,10 @@ struct tfhe_eval_key {
   double* bk_fft;   // device [n][2l][2*parts][N/2] complex (re, im), transform layout, times 2/N
   double* tw;       // device [N/2] complex twiddles of the transform tree
   uint32_t* ksk;    // device [N][t][base-1][n+1]
+  uint32_t* pks;    // device packing key [n][t][base-1][2][N], or NULL until uploaded
   int64_t bk_bytes;
   int64_t ksk_bytes;
+  int64_t pks_bytes;
 };
 
 namespace gt {
@@ -35,13 +38,14 @@ int check_params(const tfhe_params& p);
 // generator tags
 enum : uint32_t {
   kTagLweKey = 1, kTagRlweKey = 2, kTagBkMask = 3, kTagBkNoise = 4,
-  kTagKskMask = 5, kTagKskNoise = 6, kTagEncMask = 7, kTagEncNoise = 8
+  kTagKskMask = 5, kTagKskNoise = 6, kTagEncMask = 7, kTagEncNoise = 8, kTagPksMask = 9, kTagPksNoise = 10
 };
 
 // host-side cryptography (gt_host.cpp)
 uint64_t rand_word(uint64_t seed, uint32_t tag, uint64_t idx);
 uint32_t rand_noise(uint64_t seed, uint32_t tag, uint64_t idx, double alpha);
 void keygen_host(tfhe_secret_key& sk);
+void packing_keygen_host(tfhe_secret_key& sk);
 void encrypt_host(const tfhe_secret_key& sk, uint64_t seed, const uint32_t* mu, int64_t first,
                   int64_t count, uint32_t* ct);
 int key_part_shift(int parts);
@@ -100,6 +104,9 @@ int launch_mux_combine(const tfhe_eval_key* ek, uint32_t* ext, int64_t M, void* 
 // (v, o, j) selects bit o of table[2j + x[v][0]]
 int launch_lut_leaf(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits, const uint32_t* table,
                     int32_t out_bits, int64_t V, uint32_t* nodes, void* stream);
+int launch_pack_keyswitch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
+                          void* stream);
+int launch_sample_extract(int32_t N, const uint32_t* trlwe, int64_t B, int32_t K, uint32_t* out, void* stream);
 int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
                           uint32_t* c, int64_t B, void* stream);
 

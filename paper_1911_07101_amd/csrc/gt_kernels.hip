@@ -798,6 +798,93 @@ __global__ __launch_bounds__(256) void not_kernel(const uint32_t* __restrict__ i
   if (idx < words) out[idx] = 0u - in[idx];
 }
 
+// ------------------------------------- TFHE side of the cryptosystem switch
+// Functional key switching with the packing morphism (Section 3.2, step 2):
+// Z LWE samples of dimension n become one TRLWE sample (A, B) whose phase is
+// sum_z phase_z X^z.  out = (0, sum_z b_z X^z) - sum_{z,i,j} X^z PKS[i][j][v]
+// over the non-zero digits v of the rounded a_{z,i}.  pack_init writes the
+// first term; pack_ks_kernel adds the rest, one block per (TRLWE, chunk of
+// PKS_IC input coefficients), each thread owning 2N/256 output words, and
+// adds its partial sums to out with 32-bit atomic adds (exact mod 2^32, so
+// the result does not depend on their order).
+constexpr int PKS_IC = 8;       // input coefficients per block
+constexpr int PKS_ZMAX = 2048;  // Z <= N <= 2048
+
+__global__ __launch_bounds__(256) void pack_init_kernel(const uint32_t* __restrict__ lwe, int n, int N, int Z,
+                                                        int64_t B, uint32_t* __restrict__ out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= B * 2 * N) return;
+  const int64_t b = idx / (2 * N);
+  const int k = static_cast<int>(idx - b * 2 * N);
+  uint32_t w = 0u;
+  if (k >= N && k - N < Z) w = lwe[(b * Z + (k - N)) * (n + 1) + n];
+  out[idx] = w;
+}
+
+template <int N>
+__global__ __launch_bounds__(256) void pack_ks_kernel(const uint32_t* __restrict__ lwe,
+                                                      const uint32_t* __restrict__ pks, int n, int Z, int t,
+                                                      int basebit, uint32_t* __restrict__ out) {
+  constexpr int W = 2 * N / 256;  // output words per thread: k = threadIdx.x + 256 * w
+  __shared__ uint16_t s_r[PKS_IC][PKS_ZMAX];  // rounded a_{z,i} (t * basebit <= 16 bits)
+  __shared__ uint32_t s_key[3][2 * N];        // entries (i, j, v = 1..3) of the packing key
+  const int64_t b = blockIdx.x;
+  const int i0 = blockIdx.y * PKS_IC;
+  const int ic = min(PKS_IC, n - i0);
+  const int prec = t * basebit, vals = (1 << basebit) - 1;
+  const uint32_t round = prec < 32 ? (1u << (31 - prec)) : 0u;
+  for (int idx = threadIdx.x; idx < ic * Z; idx += 256) {
+    const int ii = idx / Z, z = idx - ii * Z;
+    const uint32_t a = lwe[(b * Z + z) * (n + 1) + i0 + ii];
+    s_r[ii][z] = static_cast<uint16_t>((a + round) >> (32 - prec));
+  }
+  uint32_t acc[W];
+#pragma unroll
+  for (int w = 0; w < W; w++) acc[w] = 0u;
+  for (int ii = 0; ii < ic; ii++) {
+    for (int j = 0; j < t; j++) {
+      __syncthreads();  // s_r written / the previous entries no longer read
+      const uint32_t* e = pks + (static_cast<size_t>(i0 + ii) * t + j) * vals * 2 * N;
+      for (int idx = threadIdx.x; idx < vals * 2 * N; idx += 256) s_key[idx / (2 * N)][idx % (2 * N)] = e[idx];
+      __syncthreads();
+      const int sh = (t - 1 - j) * basebit;
+      for (int z = 0; z < Z; z++) {
+        const uint32_t v = (static_cast<uint32_t>(s_r[ii][z]) >> sh) & static_cast<uint32_t>(vals);
+        if (v == 0) continue;  // uniform across the block
+        const uint32_t* key = s_key[v - 1];
+#pragma unroll
+        for (int w = 0; w < W; w++) {
+          const int k = threadIdx.x + 256 * w;  // word k of (A, B): polynomial k / N, coefficient k % N
+          const int c = k & (N - 1), base = k - c;
+          const int src = c - z;  // X^z moves coefficient src to c, negated when it wrapped
+          const uint32_t x = key[base + (src & (N - 1))];
+          acc[w] -= src < 0 ? 0u - x : x;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int w = 0; w < W; w++) atomicAdd(out + b * 2 * N + threadIdx.x + 256 * w, acc[w]);
+}
+
+// SampleExtract of coefficients 0 .. K-1 (Section 3.2, step 3): out[b][i] =
+// (a'_0 .. a'_{N-1}, B_i), a'_j = A_{i-j} (j <= i) or -A_{N+i-j} (j > i)
+__global__ __launch_bounds__(256) void sample_extract_kernel(const uint32_t* __restrict__ trlwe, int N, int64_t B,
+                                                             int K, uint32_t* __restrict__ out) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t row = N + 1;
+  if (idx >= B * K * row) return;
+  const int64_t s = idx / row;
+  const int j = static_cast<int>(idx - s * row);
+  const int64_t b = s / K;
+  const int i = static_cast<int>(s - b * K);
+  const uint32_t* A = trlwe + b * 2 * N;
+  uint32_t w;
+  if (j == N) w = A[N + i];
+  else w = j <= i ? A[i - j] : 0u - A[N + i - j];
+  out[idx] = w;
+}
+
 // Standalone negacyclic product c = d * b in Z_{2^32}[X]/(X^N+1) with the blind
 // rotation's transform code: d small signed digits, b split into S parts on
 // the device and transformed there.  One polynomial per T threads.
@@ -1000,6 +1087,35 @@ int launch_lut_leaf(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits
   hipLaunchKernelGGL(lut_leaf_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), x, ek->p.n, msg_bits, t, out_bits, V, nodes);
   return launch_status("lut_leaf_kernel");
+}
+
+int launch_pack_keyswitch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
+                          void* stream) {
+  const tfhe_params& p = ek->p;
+  if (p.ks_t * p.ks_basebit > 16 || (1 << p.ks_basebit) - 1 > 3)
+    return fail(TFHE_EUNSUPPORTED, "packing key switching needs t * basebit <= 16 and basebit <= 2");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t words = B * 2 * p.N;
+  hipLaunchKernelGGL(pack_init_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0, st, lwe,
+                     p.n, p.N, Z, B, out);
+  int rc = launch_status("pack_init_kernel");
+  if (rc) return rc;
+  dim3 grid(static_cast<unsigned>(B), static_cast<unsigned>((p.n + PKS_IC - 1) / PKS_IC));
+  switch (p.N) {
+    case 256: hipLaunchKernelGGL(pack_ks_kernel<256>, grid, dim3(256), 0, st, lwe, ek->pks, p.n, Z, p.ks_t, p.ks_basebit, out); break;
+    case 512: hipLaunchKernelGGL(pack_ks_kernel<512>, grid, dim3(256), 0, st, lwe, ek->pks, p.n, Z, p.ks_t, p.ks_basebit, out); break;
+    case 1024: hipLaunchKernelGGL(pack_ks_kernel<1024>, grid, dim3(256), 0, st, lwe, ek->pks, p.n, Z, p.ks_t, p.ks_basebit, out); break;
+    case 2048: hipLaunchKernelGGL(pack_ks_kernel<2048>, grid, dim3(256), 0, st, lwe, ek->pks, p.n, Z, p.ks_t, p.ks_basebit, out); break;
+    default: return fail(TFHE_EUNSUPPORTED, "packing key switching for N=%d", p.N);
+  }
+  return launch_status("pack_ks_kernel");
+}
+
+int launch_sample_extract(int32_t N, const uint32_t* trlwe, int64_t B, int32_t K, uint32_t* out, void* stream) {
+  const int64_t words = B * K * (N + 1);
+  hipLaunchKernelGGL(sample_extract_kernel, dim3(static_cast<unsigned>((words + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), trlwe, N, B, K, out);
+  return launch_status("sample_extract_kernel");
 }
 
 int launch_negacyclic_mul(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b, uint32_t* c,

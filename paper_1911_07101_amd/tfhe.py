@@ -70,6 +70,11 @@ _SIGNATURES = {
     "tfhe_mux_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
     "glyph_mux_lut_batch": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i32, _vp, _i64, _vp, _i64, _vp]),
     "glyph_mux_lut_workspace_bytes": (_i64, [_vp, _i64, _i32, _i32]),
+    "tfhe_packing_key_upload": (ctypes.c_int, [_vp, _vp]),
+    "tfhe_export_packing_key": (ctypes.c_int, [_vp, _vp]),
+    "tfhe_pack_keyswitch_batch": (ctypes.c_int, [_vp, _vp, _i32, _vp, _i64, _vp]),
+    "tfhe_sample_extract_batch": (ctypes.c_int, [_i32, _vp, _i64, _i32, _vp, _vp]),
+    "tfhe_torus_testvec": (ctypes.c_int, [_i32, _i32, _vp, _vp]),
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
@@ -364,6 +369,41 @@ def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspac
     _check(lib().glyph_mux_lut_batch(ek.handle, _dptr(x), msg_bits, _hptr(t), out_bits, _dptr(out), V,
                                      _dptr(ws), ws.numel(), _stream(stream)))
     return out
+
+
+def tfhe_packing_key_upload(sk: SecretKey, ek: EvalKey):
+    _check(lib().tfhe_packing_key_upload(sk.handle, ek.handle))
+
+
+def tfhe_export_packing_key(sk: SecretKey) -> np.ndarray:
+    p = sk.params
+    pks = np.zeros(p.n * p.ks_t * ((1 << p.ks_basebit) - 1) * 2 * p.N, np.uint32)
+    _check(lib().tfhe_export_packing_key(sk.handle, _hptr(pks)))
+    return pks
+
+
+def tfhe_pack_keyswitch_batch(ek: EvalKey, lwe, out=None, stream=None):
+    """lwe [B][Z][n+1] -> TRLWE samples [B][2][N] (phase sum_z phase_z X^z)."""
+    B, Z = lwe.shape[0], lwe.shape[1]
+    out = _empty((B, 2, ek.params.N), ek) if out is None else out
+    _check(lib().tfhe_pack_keyswitch_batch(ek.handle, _dptr(lwe), Z, _dptr(out), B, _stream(stream)))
+    return out
+
+
+def tfhe_sample_extract_batch(trlwe, K: int, out=None, stream=None):
+    """TRLWE samples [B][2][N] -> LWE samples of coefficients 0..K-1, [B][K][N+1]."""
+    import torch
+    B, N = trlwe.shape[0], trlwe.shape[2]
+    out = torch.empty((B, K, N + 1), dtype=torch.int32, device=trlwe.device) if out is None else out
+    _check(lib().tfhe_sample_extract_batch(N, _dptr(trlwe), B, K, _dptr(out), _stream(stream)))
+    return out
+
+
+def tfhe_torus_testvec(N: int, msg_bits: int, values) -> np.ndarray:
+    v = _host_u32(values)
+    tv = np.zeros(N, np.uint32)
+    _check(lib().tfhe_torus_testvec(N, msg_bits, _hptr(v), _hptr(tv)))
+    return tv
 
 
 def tfhe_not_batch(x, out=None, stream=None):

@@ -287,6 +287,62 @@ def test_mux_lut_toy(torch, msg_bits, out_bits):
     assert np.array_equal((dec.astype(np.int64) << np.arange(out_bits)).sum(axis=1), table[xs])
 
 
+def test_pack_keyswitch_toy(torch):
+    """Packing key switching of B = 3 sets of LWE samples (Z = N, a ragged
+    100 and 1) into TRLWE samples: bit-exact with the oracle, and coefficient
+    z of the phase decodes to message z."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    rng = np.random.default_rng(61)
+    for Z in (p["N"], 100, 1):
+        B = 3
+        m = rng.integers(0, 64, (B, Z)).astype(np.uint32)
+        lwe = tfhe.tfhe_encrypt_torus(sk, 60 + Z, (m.ravel() << 26).astype(np.uint32)).reshape(B, Z, p["n"] + 1)
+        say(f"pack keyswitch toy B={B} Z={Z}")
+        got = tfhe.to_host(tfhe.tfhe_pack_keyswitch_batch(ek, tfhe.to_device(lwe)))
+        for b in range(B):
+            assert np.array_equal(got[b], oracle.pack_keyswitch(ok, lwe[b])), (Z, b)
+            ext = np.stack([oracle.sample_extract_at(got[b], z) for z in range(Z)])
+            ph = oracle.phase(ok.S, ext).astype(np.int64)
+            assert np.array_equal(((ph + (1 << 25)) >> 26) % 64, m[b])
+
+
+def test_sample_extract_batch(torch):
+    """SampleExtract of the first K coefficients of random TRLWE samples
+    equals the oracle's extraction of each coefficient."""
+    rng = np.random.default_rng(62)
+    for N, B, K in [(256, 5, 256), (1024, 3, 7), (2048, 2, 1)]:
+        acc = rng.integers(0, M32, (B, 2, N), dtype=np.uint64).astype(np.uint32)
+        got = tfhe.to_host(tfhe.tfhe_sample_extract_batch(tfhe.to_device(acc), K))
+        for b in range(B):
+            ref = np.stack([oracle.sample_extract_at(acc[b], i) for i in range(K)])
+            assert np.array_equal(got[b], ref), (N, b)
+
+
+def test_bootstrap_onto_multiples_of_inverse_modulus_n2048(torch):
+    """Step 4 of the switch with the N = 2048 parameters: a programmable
+    bootstrap whose test polynomial holds multiples of 1/q (q = 257) maps
+    each 3-bit message m to f(m)/q; bit-exact with the oracle on a sample and
+    decoding to f(m) for all 512 inputs (before key switching)."""
+    cfg = wl.CONFIGS["lut3_n2048"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("lut3_n2048", torch)
+    q = 257
+    f = np.random.default_rng(63).integers(0, q, 8)
+    values = np.array([(int(v) * (1 << 32) + q // 2) // q for v in f], dtype=np.uint64).astype(np.uint32)
+    tv = tfhe.tfhe_torus_testvec(p["N"], 3, values)
+    assert np.array_equal(tv, oracle.torus_testvec(p["N"], 3, values))
+    m = np.arange(8, dtype=np.uint32).repeat(64)
+    ct = tfhe.tfhe_encrypt_torus(sk, 64, (m << 28).astype(np.uint32))
+    say("bootstrap onto multiples of 1/257, N=2048, 512 samples")
+    got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(ct), tfhe.to_device(tv)))
+    ph = tfhe.tfhe_decrypt_phase(sk, got, 1).astype(np.int64)
+    assert np.array_equal(((ph * q + (1 << 31)) >> 32) % q, f[m])
+    idx = np.array([0, 100, 301, 511])
+    assert np.array_equal(got[idx], oracle.bootstrap_no_ks(ok, ct[idx], tv))
+
+
 # ---------------------------------------------------- full-size workloads
 
 def test_tfhe128_nand_4096(torch):
@@ -383,6 +439,32 @@ def test_softmax_mux3_8192(torch):
     ref = oracle.mux_lut(ok, ct[idx], mb, table, ob)
     say(f"  oracle sample of {len(idx)} values in {time.time() - t0:.1f}s")
     assert np.array_equal(got[idx], ref)
+
+
+def test_switch_steps_128bit(torch):
+    """Steps 2 and 3 of the BGV-to-TFHE switch at the 128-bit parameters:
+    1024 LWE samples packed into one TRLWE sample (bit-exact with the
+    oracle), then its first 64 coefficients extracted and key-switched back
+    to dimension n, each decoding to its message."""
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    say("packing key n=630 N=1024 (library and oracle)")
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    Z = p["N"]
+    m = np.random.default_rng(65).integers(0, 16, Z).astype(np.uint32)
+    lwe = tfhe.tfhe_encrypt_torus(sk, 65, (m << 28).astype(np.uint32)).reshape(1, Z, p["n"] + 1)
+    t0 = time.time()
+    acc = tfhe.tfhe_pack_keyswitch_batch(ek, tfhe.to_device(lwe))
+    ext = tfhe.tfhe_sample_extract_batch(acc, 64)
+    back = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, ext.reshape(64, p["N"] + 1)))
+    say(f"  gpu {time.time() - t0:.2f}s")
+    ph = tfhe.tfhe_decrypt_phase(sk, back).astype(np.int64)
+    assert np.array_equal(((ph + (1 << 27)) >> 28) % 16, m[:64])
+    t0 = time.time()
+    ref = oracle.pack_keyswitch(ok, lwe[0])
+    say(f"  oracle packing in {time.time() - t0:.1f}s")
+    assert np.array_equal(tfhe.to_host(acc)[0], ref)
 
 
 def test_conv_relu_streamed(torch):

@@ -121,3 +121,19 @@ def test_transform_error_bound_covers_every_workload():
     with pytest.raises(tfhe.TfheError) as ei:
         tfhe.tfhe_transform_error_bound(dict(TOY, N=2048, l=1, bg_bit=24))
     assert ei.value.rc == tfhe.TFHE_EUNSUPPORTED
+
+
+def test_packing_key_matches_oracle():
+    """The library's packing key (host keygen, rotated sums for A*S) is
+    word-for-word the oracle's (schoolbook products)."""
+    p = dict(TOY, n=12, N=256)
+    sk = tfhe.tfhe_secret_keygen(p, 77)
+    ok = oracle.Keys(p, 77)
+    assert np.array_equal(tfhe.tfhe_export_packing_key(sk), ok.packing_key())
+
+
+def test_torus_testvec_matches_oracle():
+    rng = np.random.default_rng(12)
+    for N, bits in [(256, 3), (1024, 3), (2048, 5)]:
+        vals = rng.integers(0, 1 << 32, 1 << bits, dtype=np.uint64).astype(np.uint32)
+        assert np.array_equal(tfhe.tfhe_torus_testvec(N, bits, vals), oracle.torus_testvec(N, bits, vals))
