@@ -552,3 +552,39 @@ def test_workspace_too_small_is_rejected(torch):
     with pytest.raises(tfhe.TfheError) as ei:
         tfhe.tfhe_gate_bootstrap_batch(ek, 17, x, x)
     assert ei.value.rc == tfhe.TFHE_EINVAL
+
+
+def test_empty_and_invalid_calls(torch):
+    """Empty batches are no-ops that leave the output untouched; gate windows
+    outside the tensor, a missing packing key and bad table sizes are
+    rejected before any launch."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    row = p["n"] + 1
+    x = tfhe.to_device(np.zeros((4, row), np.uint32))
+    sentinel = torch.full((4, row), 7, dtype=torch.int32, device="cuda:0")
+    ws = tfhe.alloc_workspace(ek, 8)
+    L = tfhe.lib()
+    assert L.tfhe_gate_bootstrap_batch(ek.handle, 0, tfhe._dptr(x), tfhe._dptr(x), tfhe._dptr(sentinel), 0,
+                                       tfhe._dptr(ws), ws.numel(), None) == tfhe.TFHE_OK
+    assert L.tfhe_keyswitch_batch(ek.handle, tfhe._dptr(x), tfhe._dptr(sentinel), 0, None) == tfhe.TFHE_OK
+    assert L.tfhe_mux_batch(ek.handle, tfhe._dptr(x), tfhe._dptr(x), tfhe._dptr(x), tfhe._dptr(sentinel), 0,
+                            tfhe._dptr(ws), ws.numel(), None) == tfhe.TFHE_OK
+    torch.cuda.synchronize()
+    assert bool((sentinel == 7).all())
+    y = tfhe.to_device(np.zeros((2, 8, row), np.uint32))
+    with pytest.raises(tfhe.TfheError) as ei:  # 2 values x 7 gates: window end 15 is outside
+        tfhe.glyph_relu_batch(ek, y, 8, y=torch.empty_like(y), gate_begin=0, gate_end=15)
+    assert ei.value.rc == tfhe.TFHE_EINVAL
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.glyph_irelu_batch(ek, y, y, out=torch.empty_like(y), gate_begin=10, gate_end=9)
+    assert ei.value.rc == tfhe.TFHE_EINVAL
+    with pytest.raises(ValueError):
+        tfhe.glyph_mux_lut_batch(ek, y[:, :3], np.arange(7), 3)  # 3 selector bits need 8 entries
+    with pytest.raises(tfhe.TfheError) as ei:  # entry 9 does not fit in 3 output bits
+        tfhe.glyph_mux_lut_batch(ek, y[:, :3], np.array([0, 1, 2, 3, 4, 5, 6, 9]), 3)
+    assert ei.value.rc == tfhe.TFHE_EINVAL
+    sk2, ek2 = tfhe.tfhe_keygen_from_seed(p, 5, 0)  # fresh key without a packing key
+    with pytest.raises(tfhe.TfheError) as ei:
+        tfhe.tfhe_pack_keyswitch_batch(ek2, tfhe.to_device(np.zeros((1, 3, row), np.uint32)))
+    assert ei.value.rc == tfhe.TFHE_EINVAL
