@@ -53,8 +53,9 @@ enum {
  * ring products are computed with a floating-point transform and rounded;
  * the parameters must keep its worst-case error below 1/8 with the key split
  * into 16-bit or 11-bit signed parts (it holds for all the parameter sets
- * the library is tested on; it fails for example at N = 2048 with
- * bg_bit = 16); otherwise key generation returns TFHE_EUNSUPPORTED. */
+ * the library is tested on, with 16-bit parts; it fails for example at
+ * N = 2048 with bg_bit = 24); otherwise key generation returns
+ * TFHE_EUNSUPPORTED. */
 typedef struct {
   int32_t n;          /* LWE dimension */
   int32_t N;          /* TRLWE ring degree */
