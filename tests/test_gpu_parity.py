@@ -579,10 +579,11 @@ def test_empty_and_invalid_calls(torch):
     with pytest.raises(tfhe.TfheError) as ei:
         tfhe.glyph_irelu_batch(ek, y, y, out=torch.empty_like(y), gate_begin=10, gate_end=9)
     assert ei.value.rc == tfhe.TFHE_EINVAL
+    x3 = tfhe.to_device(np.zeros((2, 3, row), np.uint32))
     with pytest.raises(ValueError):
-        tfhe.glyph_mux_lut_batch(ek, y[:, :3], np.arange(7), 3)  # 3 selector bits need 8 entries
+        tfhe.glyph_mux_lut_batch(ek, x3, np.arange(7), 3)  # 3 selector bits need 8 entries
     with pytest.raises(tfhe.TfheError) as ei:  # entry 9 does not fit in 3 output bits
-        tfhe.glyph_mux_lut_batch(ek, y[:, :3], np.array([0, 1, 2, 3, 4, 5, 6, 9]), 3)
+        tfhe.glyph_mux_lut_batch(ek, x3, np.array([0, 1, 2, 3, 4, 5, 6, 9]), 3)
     assert ei.value.rc == tfhe.TFHE_EINVAL
     sk2, ek2 = tfhe.tfhe_keygen_from_seed(p, 5, 0)  # fresh key without a packing key
     with pytest.raises(tfhe.TfheError) as ei:
