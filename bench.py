@@ -40,10 +40,10 @@ def algorithmic_lane_ops(p, parts: int) -> float:
     n = N // 2
     outs = 2 * parts
     bfly = n // 2 * int(math.log2(n))
-    fwd = 2 * l * bfly * 8                 # complex multiply (4) + 2 complex adds (4)
+    fwd = 2 * l * bfly * 6                 # a = u + w v: 4 FMAs; b = 2u - a: 2 FMAs
     digits = 2 * l * N * 4 + 2 * N * 3     # digit extract + convert; rotation difference
     pointwise = 2 * l * outs * n * 4       # complex multiply-accumulate: 4 FMAs
-    inv = outs * bfly * 8
+    inv = outs * bfly * 8                  # u + v: 2 adds; (u - v) conj(w): 2 subs + 2 mul + 2 FMAs
     convert = 2 * N * 2 * parts            # round (1 add) and shift-add per part, accumulate
     return float(n_lwe * (fwd + digits + pointwise + inv + convert))
 

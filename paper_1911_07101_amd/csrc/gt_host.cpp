@@ -350,7 +350,10 @@ int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
 // (forward error of the digits; key rounding u2 = 2u; a complex product-sum
 // of R terms with two roundings per term and component), ||x||_2 <= D sqrt N,
 // ||y||_2 <= Y sqrt N, and ||z||_2 <= R ||x||_1 ||y||_2 <= R D N Y sqrt N
-// (Young's inequality for the negacyclic convolution).
+// (Young's inequality for the negacyclic convolution).  The device's forward
+// butterflies (a = u + w v in four FMAs, b = 2u - a in two) have a per-stage
+// relative error of at most mu + 3.02u to first order, below the theorem's
+// eta, so eta covers them.
 double transform_error_bound(const tfhe_params& p, int parts) {
   const double u = std::ldexp(1.0, -53), u2 = 2 * u;
   const int n = p.N / 2;

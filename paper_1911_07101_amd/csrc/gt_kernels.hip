@@ -180,10 +180,11 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
-          const double2 u = x[e];
-          const double2 v = cmul(x[e2], z[g]);
-          x[e] = cadd(u, v);
-          x[e2] = csub(u, v);
+          // a = u + w v with four FMAs, b = u - w v = 2u - a with two
+          const double2 u = x[e], v = x[e2], w = z[g];
+          const double2 a = make_double2(fma(w.x, v.x, fma(-w.y, v.y, u.x)), fma(w.x, v.y, fma(w.y, v.x, u.y)));
+          x[e] = a;
+          x[e2] = make_double2(fma(2.0, u.x, -a.x), fma(2.0, u.y, -a.y));
         });
       });
     });
