@@ -81,13 +81,13 @@ struct PrepArgs {
   const uint32_t* ca;  // gate: first operand; plain: the input; relu: x; irelu: u; mux: selectors
   const uint32_t* cb;  // gate: second operand; irelu: delta; mux: if-true; mux tree: the level's children
   int64_t B;
-  int32_t bits;        // relu: bits of x; irelu: bits of delta; mux tree: selector bits per value
-  int64_t gate_begin;  // relu, irelu
-  int32_t sign_bits;   // irelu: bits of u (its sign is bit sign_bits - 1)
-  const uint32_t* cc;  // mux: if-false
-  int64_t group;       // mux tree: nodes per (value, output bit) at this level
-  int32_t out_bits;    // mux tree: output bits per value
-  int32_t level;       // mux tree: selector bit of this level
+  int32_t bits = 0;           // relu: bits of x; irelu: bits of delta; mux tree: selector bits per value
+  int64_t gate_begin = 0;     // relu, irelu
+  int32_t sign_bits = 0;      // irelu: bits of u (its sign is bit sign_bits - 1)
+  const uint32_t* cc = nullptr;  // mux: if-false
+  int64_t group = 0;          // mux tree: nodes per (value, output bit) at this level
+  int32_t out_bits = 0;       // mux tree: output bits per value
+  int32_t level = 0;          // mux tree: selector bit of this level
 };
 
 int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws, void* stream);

@@ -482,10 +482,12 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
 
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
-      // recompute the rotation indices for each q instead of keeping 2E of
-      // them live across the transforms (the empty asm hides a_i's value)
+      // recompute the rotation indices and coefficient positions for each q
+      // instead of keeping 4E of them live across the transforms (the empty
+      // asm hides the values of a_i and t)
       uint32_t a_q = a_i;
-      asm volatile("" : "+v"(a_q));
+      int t_q = t;
+      asm volatile("" : "+v"(a_q), "+v"(t_q));
       // D = X^{a_i} P - P (plus the decomposition offset) at coefficients
       // t + T*e (h = 0) and t + T*e + NR/2 (h = 1): point e's real and imaginary part
       uint32_t D[2][E];
@@ -493,7 +495,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
       for (int e = 0; e < E; e++)
 #pragma unroll
         for (int h = 0; h < 2; h++) {
-          const int j = t + T * e + h * NC;
+          const int j = t_q + T * e + h * NC;
           D[h][e] = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
         }
       for (int jj = 0; jj < l; jj++) {
@@ -552,11 +554,13 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
   // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0)
   if (active) {
     uint32_t* out = extract + c * (NR + 1);
+    int t_x = t;  // hidden so that no coefficient position stays live over the CMux loop
+    asm volatile("" : "+v"(t_x));
 #pragma unroll
     for (int e = 0; e < E; e++)
 #pragma unroll
       for (int h = 0; h < 2; h++) {
-        const int j = t + T * e + h * NC;
+        const int j = t_x + T * e + h * NC;
         out[j] = j == 0 ? acc_a[0] : 0u - acc_a[NR - j];
       }
     if (t == 0) out[NR] = acc_b[0];
@@ -588,18 +592,16 @@ constexpr int KS_COLS = 64;  // output columns per block (one wave)
 constexpr int KS_ICH = 16;   // input coefficients staged per round
 constexpr int KS_MAXROWS = 64;  // t * 2^basebit rows of one coefficient, at most
 
-// KT > 0: digit count and base fixed at compile time (the digit loop unrolls);
-// KT = 0: runtime ks_t / basebit.  MAXROWS >= ks_t * 2^basebit.
-template <int MAXROWS, int KT, int KBB>
+// Any digit count and base with ks_t * 2^basebit <= MAXROWS (the specialised
+// kernel below covers t = 8, base 4).
+template <int MAXROWS>
 __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restrict__ in,
                                                        const uint32_t* __restrict__ ksk,
                                                        uint32_t* __restrict__ out, int n, int N,
-                                                       int ks_t_rt, int basebit_rt, int64_t B, int mode,
+                                                       int ks_t, int basebit, int64_t B, int mode,
                                                        int32_t bits, int64_t gate_begin) {
   __shared__ uint32_t s_in[KS_CB][KS_ICH];
   __shared__ uint32_t s_rows[2][MAXROWS][KS_COLS];
-  const int ks_t = KT > 0 ? KT : ks_t_rt;
-  const int basebit = KT > 0 ? KBB : basebit_rt;
   const int lane = threadIdx.x;
   const int64_t c0 = static_cast<int64_t>(blockIdx.x) * KS_CB;
   const int col = blockIdx.y * KS_COLS + lane;
@@ -651,28 +653,13 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
       const bool more = ii + 1 < iend;
       if (more) fetch(i0 + ii + 1);
       const uint32_t* rows = &s_rows[b][0][lane];
-      if constexpr (KT > 0) {
-#pragma unroll 8
-        for (int k = 0; k < KS_CB; k++) {
-          const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
-          const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
-          uint32_t sum = 0u;
-#pragma unroll
-          for (int j = 0; j < KT; j++) {
-            const uint32_t v = (r >> ((KT - 1 - j) * KBB)) & ((1u << KBB) - 1u);
-            sum += rows[((j << KBB) + v) * KS_COLS];
-          }
-          acc[k] -= sum;
-        }
-      } else {
 #pragma unroll 4
-        for (int k = 0; k < KS_CB; k++) {
-          const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
-          const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
-          for (int j = 0; j < ks_t; j++) {
-            const uint32_t v = (r >> ((ks_t - 1 - j) * basebit)) & static_cast<uint32_t>(vals);
-            acc[k] -= rows[(j * base + v) * KS_COLS];
-          }
+      for (int k = 0; k < KS_CB; k++) {
+        const uint32_t x = __builtin_amdgcn_readfirstlane(s_in[k][ii]);
+        const uint32_t r = prec == 32 ? x : (x + round) >> (32 - prec);
+        for (int j = 0; j < ks_t; j++) {
+          const uint32_t v = (r >> ((ks_t - 1 - j) * basebit)) & static_cast<uint32_t>(vals);
+          acc[k] -= rows[(j * base + v) * KS_COLS];
         }
       }
       if (more) put(b ^ 1);
@@ -1046,10 +1033,10 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
     hipLaunchKernelGGL(keyswitch_t8b2_kernel, g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
                        bits, gate_begin);
   } else if (p.ks_t * (1 << p.ks_basebit) <= 32)
-    hipLaunchKernelGGL((keyswitch_kernel<32, 0, 0>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
+    hipLaunchKernelGGL((keyswitch_kernel<32>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
                        p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   else
-    hipLaunchKernelGGL((keyswitch_kernel<64, 0, 0>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
+    hipLaunchKernelGGL((keyswitch_kernel<64>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
                        p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
   return launch_status("keyswitch_kernel");
 }
