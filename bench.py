@@ -43,7 +43,11 @@ def algorithmic_lane_ops(p, parts: int) -> float:
     fwd = 2 * l * bfly * 6                 # a = u + w v: 4 FMAs; b = 2u - a: 2 FMAs
     digits = 2 * l * N * 4 + 2 * N * 3     # digit extract + convert; rotation difference
     pointwise = 2 * l * outs * n * 4       # complex multiply-accumulate: 4 FMAs
-    inv = outs * bfly * 8                  # u + v: 2 adds; (u - v) conj(w): 2 subs + 2 mul + 2 FMAs
+    # cyclic inverse by decimation in time: butterflies with twiddle 1 or -i
+    # (n/2 at the first stage, n/2^s at stage s >= 1) take 4 adds, the others
+    # 6 FMAs; then the twist, one complex product (4 ops) per point
+    trivial = n // 2 + sum(n >> s for s in range(1, int(math.log2(n))))
+    inv = outs * (bfly * 6 - trivial * 2 + n * 4)
     convert = 2 * N * 2 * parts            # round (1 add) and shift-add per part, accumulate
     return float(n_lwe * (fwd + digits + pointwise + inv + convert))
 

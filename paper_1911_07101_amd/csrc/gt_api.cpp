@@ -201,9 +201,10 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   // [n][2l][2 * parts][N/2] complex doubles
   ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
   ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
-  const int64_t tw_bytes = static_cast<int64_t>(p.N / 2) * 16;
+  // forward tree twiddles, inverse stage twiddles, twist: N/2 complex each
+  const int64_t tw_bytes = static_cast<int64_t>(3 * (p.N / 2)) * 16;
 
-  std::vector<double> bk_host, tw(static_cast<size_t>(p.N));
+  std::vector<double> bk_host, tw(static_cast<size_t>(3 * p.N));
   try {
     bk_host.resize(static_cast<size_t>(ek->bk_bytes / 8));
   } catch (const std::bad_alloc&) {

@@ -342,18 +342,22 @@ int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
 // (Higham, Accuracy and Stability of Numerical Algorithms, Thm 24.2)
 // ||fl(F v) - F v||_2 <= eps ||F v||_2, eps = m eta / (1 - m eta),
 // eta = mu + gamma4 (sqrt2 + mu), m = log2 n, mu <= u the twiddle error.
+// G is a radix-2 cyclic inverse transform (m stages) followed by a diagonal
+// of unit-modulus twists, one more multiplication stage of the same kind,
+// so ||fl(G P) - G P||_2 <= eps' ||G P||_2, eps' = (m+1) eta / (1 - (m+1) eta).
 // Then, with ||.||_1 of a Hadamard product bounded by Cauchy-Schwarz,
 //   ||z^ - z||_inf <= ||fl(G P) - G P||_2 + ||G (P - P_exact)||_inf
-//                  <= eps (||z||_2 + sqrt(n) E_P) + E_P,
+//                  <= eps' (||z||_2 + sqrt(n) E_P) + E_P,
 //   E_P = ||P - P_exact||_1
 //       <= R [eps (1 + u2) + u2 + gamma_2R (1 + eps)(1 + u2)] ||x||_2 ||y||_2
 // (forward error of the digits; key rounding u2 = 2u; a complex product-sum
 // of R terms with two roundings per term and component), ||x||_2 <= D sqrt N,
 // ||y||_2 <= Y sqrt N, and ||z||_2 <= R ||x||_1 ||y||_2 <= R D N Y sqrt N
-// (Young's inequality for the negacyclic convolution).  The device's forward
-// butterflies (a = u + w v in four FMAs, b = 2u - a in two) have a per-stage
-// relative error of at most mu + 3.02u to first order, below the theorem's
-// eta, so eta covers them.
+// (Young's inequality for the negacyclic convolution).  The device's
+// butterflies (a = u + w v in four FMAs, b = 2u - a in two, in both
+// directions) have a per-stage relative error of at most mu + 3.02u to first
+// order, below the theorem's eta, so eta covers them; the twist is one
+// complex product per point, also within eta.
 double transform_error_bound(const tfhe_params& p, int parts) {
   const double u = std::ldexp(1.0, -53), u2 = 2 * u;
   const int n = p.N / 2;
@@ -361,6 +365,7 @@ double transform_error_bound(const tfhe_params& p, int parts) {
   const double gamma4 = 4 * u / (1 - 4 * u);
   const double eta = u + gamma4 * (std::sqrt(2.0) + u);
   const double eps = m * eta / (1 - m * eta);
+  const double eps_inv = (m + 1) * eta / (1 - (m + 1) * eta);
   const double R = 2.0 * p.l;
   const double g2R = 2 * R * u / (1 - 2 * R * u);
   const double D = std::ldexp(1.0, p.bg_bit - 1);
@@ -369,7 +374,7 @@ double transform_error_bound(const tfhe_params& p, int parts) {
   const double x1 = D * N, x2 = D * sN, y2 = Y * sN;
   const double z2 = R * x1 * y2;
   const double ep = R * (eps * (1 + u2) + u2 + g2R * (1 + eps) * (1 + u2)) * x2 * y2;
-  return eps * (z2 + std::sqrt(static_cast<double>(n)) * ep) + ep;
+  return eps_inv * (z2 + std::sqrt(static_cast<double>(n)) * ep) + ep;
 }
 
 int key_parts(const tfhe_params& p) {
@@ -385,10 +390,27 @@ void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, d
 }
 
 void twiddles_host(int N, double* tw) {
+  const int n = N / 2;
+  const long double pi = 3.141592653589793238462643383279502884L;
+  auto put = [tw](int slot, long double re, long double im) {
+    tw[2 * slot] = static_cast<double>(re);
+    tw[2 * slot + 1] = static_cast<double>(im);
+  };
+  // [0, n): the forward's tree twiddles
   const std::vector<ComplexL> t = twiddles_long(N);
-  for (int k = 0; k < N / 2; k++) {
-    tw[2 * k] = static_cast<double>(t[k].re);
-    tw[2 * k + 1] = static_cast<double>(t[k].im);
+  for (int k = 0; k < n; k++) put(k, t[k].re, t[k].im);
+  // [n, 2n - 1): inverse stage s, entry c < 2^s at n + 2^s - 1 + c:
+  // e^{-2 pi i c / 2^(s+1)}; slot 2n - 1 is unused
+  for (int half = 1; half < n; half *= 2)
+    for (int c = 0; c < half; c++) {
+      const long double ang = -pi * static_cast<long double>(c) / static_cast<long double>(half);
+      put(n + half - 1 + c, cosl(ang), sinl(ang));
+    }
+  put(2 * n - 1, 1.0L, 0.0L);
+  // [2n, 3n): the twist zeta0^{-k} = e^{-i pi k / N} of output k
+  for (int k = 0; k < n; k++) {
+    const long double ang = -pi * static_cast<long double>(k) / static_cast<long double>(N);
+    put(2 * n + k, cosl(ang), sinl(ang));
   }
 }
 

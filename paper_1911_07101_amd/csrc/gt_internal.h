@@ -21,7 +21,7 @@ struct tfhe_eval_key {
   int device;
   int parts;        // the key's coefficients are split into 2 (16-bit) or 3 (11-bit) signed parts
   double* bk_fft;   // device [n][2l][2*parts][N/2] complex (re, im), transform layout, times 2/N
-  double* tw;       // device [N/2] complex twiddles of the transform tree
+  double* tw;       // device [3][N/2] complex: forward tree twiddles, inverse stage twiddles, twist
   uint32_t* ksk;    // device [N][t][base-1][n+1]
   uint32_t* pks;    // device packing key [n][t][base-1][2][N], or NULL until uploaded
   int64_t bk_bytes;

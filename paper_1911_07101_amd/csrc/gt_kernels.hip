@@ -50,9 +50,6 @@ __device__ __forceinline__ void static_for(F&& f) {
 __device__ __forceinline__ double2 cmul(double2 a, double2 w) {
   return make_double2(fma(a.x, w.x, -(a.y * w.y)), fma(a.x, w.y, a.y * w.x));
 }
-__device__ __forceinline__ double2 cmul_conj(double2 a, double2 w) {  // a * conj(w)
-  return make_double2(fma(a.x, w.x, a.y * w.y), fma(a.y, w.x, -(a.x * w.y)));
-}
 __device__ __forceinline__ double2 cadd(double2 a, double2 b) { return make_double2(a.x + b.x, a.y + b.y); }
 __device__ __forceinline__ double2 csub(double2 a, double2 b) { return make_double2(a.x - b.x, a.y - b.y); }
 __device__ __forceinline__ void cmac(double2& acc, double2 a, double2 w) {
@@ -151,6 +148,15 @@ __device__ __forceinline__ double2 twiddle(int t, const double2* __restrict__ tw
     return tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
 }
 
+// Cooley-Tukey butterfly (xe, xe2) <- (u + w v, u - w v): a = u + w v in four
+// FMAs, b = 2u - a in two
+__device__ __forceinline__ void ct_butterfly(double2& xe, double2& xe2, double2 w) {
+  const double2 u = xe, v = xe2;
+  const double2 a = make_double2(fma(w.x, v.x, fma(-w.y, v.y, u.x)), fma(w.x, v.y, fma(w.y, v.x, u.y)));
+  xe = a;
+  xe2 = make_double2(fma(2.0, u.x, -a.x), fma(2.0, u.y, -a.y));
+}
+
 // Forward transform of the folded polynomial over C[X]/(X^n - i)
 // (Cooley-Tukey butterflies; the block of point j at stage s splits tree node
 // k = n/2^(s+1) + j/2^(s+1) and multiplies by tw[k]).  In: pass-0 (coefficient)
@@ -180,25 +186,46 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
-          // a = u + w v with four FMAs, b = u - w v = 2u - a with two
-          const double2 u = x[e], v = x[e2], w = z[g];
-          const double2 a = make_double2(fma(w.x, v.x, fma(-w.y, v.y, u.x)), fma(w.x, v.y, fma(w.y, v.x, u.y)));
-          x[e] = a;
-          x[e2] = make_double2(fma(2.0, u.x, -a.x), fma(2.0, u.y, -a.y));
+          ct_butterfly(x[e], x[e2], z[g]);
         });
       });
     });
   });
 }
 
-// Inverse transforms without the 1/n factor (Gentleman-Sande butterflies with
-// the conjugate twiddles) of polynomials x[K0 .. K0+K) at once: they share
-// each stage's twiddles, and one polynomial's transpose is in flight while
-// another's butterflies run.  In: transform layout; out: coefficient layout.
-template <class Lay, bool TW_PERMUTED, int K0, int K, int M>
-__device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, double2* scr,
-                                            const double2* __restrict__ tw,
-                                            const double2* __restrict__ tw_uniform) {
+// Butterfly of the inverse's stages s < 3 in the pass whose window starts at
+// bit 0: the twiddle w^{-g} of order 2^(s+1) is e^{-i pi q/4}, q = g 2^(2-s),
+// a constant (1 and -i take no multiplication)
+template <int s, int g>
+__device__ __forceinline__ void dit_const_butterfly(double2& xe, double2& xe2) {
+  constexpr int q = g << (2 - s);
+  constexpr double r = 0.70710678118654757;  // 1/sqrt(2) rounded to nearest
+  const double2 u = xe, v = xe2;
+  if constexpr (q == 0) {
+    xe = cadd(u, v);
+    xe2 = csub(u, v);
+  } else if constexpr (q == 2) {  // -i v = (v.y, -v.x)
+    xe = make_double2(u.x + v.y, u.y - v.x);
+    xe2 = make_double2(u.x - v.y, u.y + v.x);
+  } else {
+    ct_butterfly(xe, xe2, make_double2(q == 1 ? r : -r, -r));
+  }
+}
+
+// Inverse transforms without the 1/n factor of polynomials x[K0 .. K0+K).
+// The forward transform leaves at tree position j the value at the root
+// zeta0 w^m of X^n = i with m the bit reversal of j (w = e^{2 pi i/n},
+// zeta0 = e^{i pi/(2n)}), so the inverse is a cyclic inverse DFT by
+// decimation in time (bit-reversed in, natural out; stage s is the butterfly
+// (u, v) -> (u + t v, u - t v) on positions j, j + 2^s with
+// t = e^{-2 pi i (j mod 2^s) / 2^(s+1)}) followed by the twist zeta0^{-k} of
+// output k, which the caller applies.  The twiddles of stage s are
+// entry 2^s - 1 + c of the table itw, c = j mod 2^s, read as itw(lane part
+// of the index, constant part); the polynomials share them, and one
+// polynomial's transpose is in flight while another's butterflies run.
+// In: transform layout; out: coefficient layout.
+template <class Lay, int K0, int K, int M, class Tab>
+__device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, double2* scr, const Tab& itw) {
   static_assert(K0 + K <= M, "polynomial range");
   constexpr int E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
@@ -210,26 +237,31 @@ __device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, doub
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::lo(p) + decltype(SI)::value;
       constexpr int b = s - w;
-      constexpr int G = E >> (b + 1);
-      double2 z[G];
-      static_for<0, G>([&](auto GI) {
-        constexpr int g = decltype(GI)::value;
-        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform);
-      });
-      static_for<K0, K0 + K>([&](auto KI) {
-        constexpr int k = decltype(KI)::value;
-        static_for<0, G>([&](auto GI) {
-          constexpr int g = decltype(GI)::value;
-          static_for<0, (1 << b)>([&](auto LI) {
-            constexpr int e = (g << (b + 1)) | decltype(LI)::value;
-            constexpr int e2 = e | (1 << b);
-            const double2 u = x[k][e];
-            const double2 v = x[k][e2];
-            x[k][e] = cadd(u, v);
-            x[k][e2] = cmul_conj(csub(u, v), z[g]);
+      constexpr int NG = 1 << b;  // twiddles per thread: one per value of the element bits below b
+      if constexpr (w == 0) {
+        static_for<K0, K0 + K>([&](auto KI) {
+          constexpr int k = decltype(KI)::value;
+          static_for<0, E>([&](auto EI) {
+            constexpr int e = decltype(EI)::value;
+            if constexpr ((e & NG) == 0) dit_const_butterfly<s, e & (NG - 1)>(x[k][e], x[k][e | NG]);
           });
         });
-      });
+      } else {
+        // position j mod 2^s = (t mod 2^w) | ((e mod 2^b) << w)
+        double2 z[NG];
+        const int lane = t & ((1 << w) - 1);
+        static_for<0, NG>([&](auto GI) {
+          constexpr int g = decltype(GI)::value;
+          z[g] = itw(lane, (1 << s) - 1 + (g << w));
+        });
+        static_for<K0, K0 + K>([&](auto KI) {
+          constexpr int k = decltype(KI)::value;
+          static_for<0, E>([&](auto EI) {
+            constexpr int e = decltype(EI)::value;
+            if constexpr ((e & NG) == 0) ct_butterfly(x[k][e], x[k][e | NG], z[e & (NG - 1)]);
+          });
+        });
+      }
     });
   });
 }
@@ -386,7 +418,12 @@ struct BrCfg {
   static constexpr int CPB = T > 64 ? 1 : 512 / T;
   static constexpr int THREADS = CPB * T;
   static constexpr int SCR = Lay::SCR;
-  static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4;
+  // the inverse's stage twiddles (NC - 1) get an LDS copy when the block is
+  // the CU's only one; a one-ciphertext block reads them from global memory
+  // (L1) so that three blocks still fit in a CU.  The twist (read once per
+  // output point and CMux) is always read from global memory.
+  static constexpr bool ITW_LDS = CPB > 1;
+  static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4 + (ITW_LDS ? (NC - 1) * 16 : 0);
   static_assert(LDS_BYTES <= 160 * 1024, "block exceeds the CU's LDS");
   // compiled for two waves per SIMD (256 VGPRs per wave)
   static constexpr int MIN_WAVES = 2;
@@ -403,6 +440,20 @@ __device__ __forceinline__ double2 load_b128(__amdgpu_buffer_rsrc_t r, uint32_t 
   return d;
 }
 
+// entry lane + k of a complex table: in LDS or global memory by pointer, or
+// through a buffer resource (lane offset in a VGPR, the constant k folded
+// into the instruction's offset)
+struct PtrTable {
+  const double2* p;
+  __device__ __forceinline__ double2 operator()(int lane, int k) const { return p[lane + k]; }
+};
+struct BufTable {
+  __amdgpu_buffer_rsrc_t r;
+  __device__ __forceinline__ double2 operator()(int lane, int k) const {
+    return load_b128(r, static_cast<uint32_t>(lane) * 16u, static_cast<uint32_t>(k) * 16u);
+  }
+};
+
 template <int LOGN, int S>
 __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAVES)) void blind_rotate_kernel(
     const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
@@ -414,6 +465,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
   __shared__ double2 s_tw[NC];
   __shared__ double2 s_scr[CPB * Lay::SCR];
   __shared__ uint32_t s_acc[CPB * 2 * NR];
+  __shared__ double2 s_itw[C::ITW_LDS ? NC - 1 : 1];
 
   const int slot = threadIdx.x / T;
   const int t = threadIdx.x % T;
@@ -421,7 +473,18 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
   const bool active = c < B;
   if (!active) c = B - 1;  // idle slots repeat the last sample and write nothing
 
+  // tw_g: [0, NC) the forward's tree twiddles, [NC, 2NC - 1) the inverse's
+  // stage twiddles, [2NC, 3NC) the twist
   for (int k = threadIdx.x; k < NC; k += C::THREADS) s_tw[tw_lds_slot<Lay>(k)] = tw_g[k];
+  if constexpr (C::ITW_LDS)
+    for (int k = threadIdx.x; k < NC - 1; k += C::THREADS) s_itw[k] = tw_g[NC + k];
+  const auto itw = [&] {
+    if constexpr (C::ITW_LDS)
+      return PtrTable{s_itw};
+    else
+      return BufTable{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + NC), 0, NC * 16, 0x00020000)};
+  }();
+  const BufTable twist{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + 2 * NC), 0, NC * 16, 0x00020000)};
   __syncthreads();
   double2* scr = s_scr + slot * Lay::SCR;
   uint32_t* acc_a = s_acc + slot * 2 * NR;
@@ -527,22 +590,24 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
     }
 
     // inverse transforms two at a time (O is even)
-    static_for<0, O / 2>([&](auto PI) {
-      fft_inverse<Lay, true, 2 * decltype(PI)::value, 2>(acc, t, scr, s_tw, tw_g);
-    });
-    // every output is within 1/8 of an integer (the transform's error bound):
-    // round, take it mod 2^32 and recombine the key parts
+    static_for<0, O / 2>([&](auto PI) { fft_inverse<Lay, 2 * decltype(PI)::value, 2>(acc, t, scr, itw); });
+    // twist, then every output is within 1/8 of an integer (the transform's
+    // error bound): round, take it mod 2^32 and recombine the key parts
+    int t_r = t;
+    asm volatile("" : "+v"(t_r));
 #pragma unroll
     for (int e = 0; e < E; e++) {
+      const int j = t_r + T * e;
+      const double2 tau = twist(t_r, T * e);
       uint32_t ra0 = 0u, ra1 = 0u, rb0 = 0u, rb1 = 0u;
 #pragma unroll
       for (int sp = S - 1; sp >= 0; sp--) {
-        ra0 = (ra0 << C::SHIFT) + round_low32(acc[sp][e].x);
-        ra1 = (ra1 << C::SHIFT) + round_low32(acc[sp][e].y);
-        rb0 = (rb0 << C::SHIFT) + round_low32(acc[S + sp][e].x);
-        rb1 = (rb1 << C::SHIFT) + round_low32(acc[S + sp][e].y);
+        const double2 va = cmul(acc[sp][e], tau), vb = cmul(acc[S + sp][e], tau);
+        ra0 = (ra0 << C::SHIFT) + round_low32(va.x);
+        ra1 = (ra1 << C::SHIFT) + round_low32(va.y);
+        rb0 = (rb0 << C::SHIFT) + round_low32(vb.x);
+        rb1 = (rb1 << C::SHIFT) + round_low32(vb.y);
       }
-      const int j = t + T * e;
       acc_a[j] += ra0;
       acc_a[j + NC] += ra1;
       acc_b[j] += rb0;
@@ -922,18 +987,20 @@ __global__ __launch_bounds__(256) void negacyclic_mul_kernel(const double2* __re
       const double2 pr = cmul(xd[e], xb[sp][e]);
       xb[sp][e] = make_double2(pr.x / NC, pr.y / NC);  // exact: NC is a power of two
     }
-    fft_inverse<Lay, false, sp, 1>(xb, t, scr, tw, tw);
+    fft_inverse<Lay, sp, 1>(xb, t, scr, PtrTable{tw + NC});
   });
   if (!active) return;
 #pragma unroll
   for (int e = 0; e < E; e++) {
+    const int j = t + T * e;
+    const double2 tau = tw[2 * NC + j];
     uint32_t r0 = 0u, r1 = 0u;
 #pragma unroll
     for (int sp = S - 1; sp >= 0; sp--) {
-      r0 = (r0 << SHIFT) + round_low32(xb[sp][e].x);
-      r1 = (r1 << SHIFT) + round_low32(xb[sp][e].y);
+      const double2 v = cmul(xb[sp][e], tau);
+      r0 = (r0 << SHIFT) + round_low32(v.x);
+      r1 = (r1 << SHIFT) + round_low32(v.y);
     }
-    const int j = t + T * e;
     c[k * NR + j] = r0;
     c[k * NR + j + NC] = r1;
   }
