@@ -80,6 +80,18 @@ def measured_traffic(digest: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def host_cpu_model() -> str:
+    """The host CPU's model name (Linux /proc/cpuinfo), else the machine type."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(cfg, ca, cb, gpu_out):
     import numpy as np
 
@@ -97,7 +109,8 @@ def cpu_baseline(cfg, ca, cb, gpu_out):
         "value": count / dt, "unit": "bootstraps/s", "cores": threads, "kind": "oracle",
         "sample": f"first {count} {cfg['gate']} gates of the batch (schoolbook products, "
                   f"OpenMP over gates), {dt:.1f} s wall",
-        "host_cpu": platform.processor() or platform.machine(),
+        "host_cpu": host_cpu_model(),
+        "core_seconds_per_bootstrap": dt * threads / count,
         "matches_gpu": bool(np.array_equal(ref, tfhe.to_host(gpu_out)[:count])),
     }
 

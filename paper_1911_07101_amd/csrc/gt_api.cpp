@@ -192,6 +192,7 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   if (!ek) return fail(TFHE_ENOMEM, "host allocation failed");
   ek->p = p;
   ek->device = device;
+  ek->cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
   ek->parts = key_parts(p);
   ek->bk_fft = nullptr;
   ek->tw = nullptr;

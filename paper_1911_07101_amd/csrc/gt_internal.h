@@ -20,6 +20,7 @@ struct tfhe_eval_key {
   tfhe_params p;
   int device;
   int parts;        // the key's coefficients are split into 2 (16-bit) or 3 (11-bit) signed parts
+  int cus;          // compute units of the device (the blind rotation sizes its blocks by it)
   double* bk_fft;   // device [n][2l][2*parts][N/2] complex (re, im), transform layout, times 2/N
   double* tw;       // device [3][N/2] complex: forward tree twiddles, inverse stage twiddles, twist
   uint32_t* ksk;    // device [N][t][base-1][n+1]

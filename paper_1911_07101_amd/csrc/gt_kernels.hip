@@ -401,7 +401,7 @@ __global__ __launch_bounds__(256) void lut_leaf_kernel(const uint32_t* __restric
 
 // ------------------------------------------------------ blind rotation
 // Ring degree 2^LOGN, key coefficients split into S signed parts.
-template <int LOGN, int S>
+template <int LOGN, int S, int WPB>
 struct BrCfg {
   using Lay = RingLayout<LOGN, S>;
   static constexpr int NR = 1 << LOGN;  // ring degree
@@ -409,20 +409,21 @@ struct BrCfg {
   static constexpr int E = Lay::E, T = Lay::T;
   static constexpr int O = 2 * S;       // transform-domain accumulators: (mask, body) x parts
   static constexpr int SHIFT = S == 2 ? 16 : 11;
-  // ciphertexts per block: 512 threads while a ciphertext fits in one wave
-  // (8 per block at N = 1024, one block per CU: the 8 ciphertexts run the
+  // ciphertexts per block: WPB waves' worth (at least one ciphertext).  A
+  // large batch takes 8 waves per block (8 ciphertexts at N = 1024, 4 at
+  // N = 2048 with two waves each; one block per CU: its ciphertexts run the
   // same CMux and share its key reads in L1, measured 4 % faster than two
-  // blocks of 4), else one ciphertext per block (its waves synchronise
-  // between transform passes, and a small block leaves room in LDS for more
-  // of them per CU)
-  static constexpr int CPB = T > 64 ? 1 : 512 / T;
+  // blocks of 4 at N = 1024 and 2.6 % faster than three blocks of 1 at
+  // N = 2048); a batch too small to give every CU a block of 8 waves takes
+  // smaller blocks, which spread it over more CUs (launch_br)
+  static constexpr int CPB = WPB * 64 / T > 0 ? WPB * 64 / T : 1;
   static constexpr int THREADS = CPB * T;
   static constexpr int SCR = Lay::SCR;
-  // the inverse's stage twiddles (NC - 1) get an LDS copy when the block is
-  // the CU's only one; a one-ciphertext block reads them from global memory
-  // (L1) so that three blocks still fit in a CU.  The twist (read once per
-  // output point and CMux) is always read from global memory.
-  static constexpr bool ITW_LDS = CPB > 1;
+  // the inverse's stage twiddles (NC - 1) get an LDS copy when a ciphertext
+  // takes one wave; at N = 2048 they do not fit beside four ciphertexts and
+  // are read from global memory (L1).  The twist (read once per output point
+  // and CMux) is always read from global memory.
+  static constexpr bool ITW_LDS = CPB > 1 && T <= 64;
   static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4 + (ITW_LDS ? (NC - 1) * 16 : 0);
   static_assert(LDS_BYTES <= 160 * 1024, "block exceeds the CU's LDS");
   // compiled for two waves per SIMD (256 VGPRs per wave)
@@ -454,12 +455,12 @@ struct BufTable {
   }
 };
 
-template <int LOGN, int S>
-__global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAVES)) void blind_rotate_kernel(
+template <int LOGN, int S, int WPB>
+__global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB>::MIN_WAVES)) void blind_rotate_kernel(
     const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
     int64_t B) {
-  using C = BrCfg<LOGN, S>;
+  using C = BrCfg<LOGN, S, WPB>;
   using Lay = typename C::Lay;
   constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
   __shared__ double2 s_tw[NC];
@@ -529,10 +530,19 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
   // key of one CMux: [2l][O][E][T] points; lane t reads point (r, o, e, t)
   const uint32_t voff = static_cast<uint32_t>(t) * 16u;
 
+  // One block barrier per CMux keeps the block's ciphertexts on the same
+  // CMux: they then read the same key points close together in time, which
+  // the L1 cache serves.  The upper half of the block's waves takes it after
+  // its first forward transform instead of at the start of the CMux, so the
+  // two waves sharing a SIMD (waves w and w + 4) run one transform apart and
+  // one's butterflies overlap the other's LDS waits.  Every wave passes one
+  // barrier per CMux (there are 2l >= 2 forward transforms per CMux).
+  constexpr bool kCmuxBarrier = CPB > 1 && T <= 64;
+  const bool late_barrier = kCmuxBarrier && CPB * T == 512 && (__builtin_amdgcn_readfirstlane(threadIdx.x) >> 8) != 0;
   for (int i = 0; i < n; i++) {
-    // keep the block's ciphertexts on the same CMux: they then read the same
-    // key points close together in time, which the L1 cache serves
-    if constexpr (CPB > 1 && T <= 64) __syncthreads();
+    if constexpr (kCmuxBarrier)
+      if (!late_barrier) __syncthreads();
+    bool first_forward = true;
     const uint32_t a_i = ab[i];
     const __amdgpu_buffer_rsrc_t bkr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
@@ -577,6 +587,9 @@ __global__ __launch_bounds__((BrCfg<LOGN, S>::THREADS), (BrCfg<LOGN, S>::MIN_WAV
           x[e] = make_double2(static_cast<double>(static_cast<int32_t>(D[0][e] << lsh) >> rsh),
                               static_cast<double>(static_cast<int32_t>(D[1][e] << lsh) >> rsh));
         fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
+        if constexpr (kCmuxBarrier)
+          if (late_barrier && first_forward) __syncthreads();
+        first_forward = false;
 #pragma unroll
         for (int o = 0; o < O; o++) {
           if (o > 0) {
@@ -1012,15 +1025,39 @@ inline int launch_status(const char* what) {
   return TFHE_OK;
 }
 
+template <int LOGN, int S, int WPB>
+int launch_br_blocks(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
+                     hipStream_t st) {
+  using C = BrCfg<LOGN, S, WPB>;
+  const int64_t blocks = (B + C::CPB - 1) / C::CPB;
+  hipLaunchKernelGGL((blind_rotate_kernel<LOGN, S, WPB>), dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS),
+                     0, st, reinterpret_cast<const double2*>(ek->bk_fft), reinterpret_cast<const double2*>(ek->tw),
+                     ws.abar, testvec, ws.extract, ek->p.n, ek->p.l, ek->p.bg_bit, B);
+  return launch_status("blind_rotate_kernel");
+}
+
+// Blocks of 8 waves when the batch fills every CU with one (or more), else
+// the largest of 4, 2, 1 waves per block that still gives every CU a block:
+// a small batch then runs one or two waves per SIMD, where its CMux chain is
+// shortest.  A ciphertext of two or four waves takes blocks of 8 waves or of
+// one ciphertext.
 template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
               hipStream_t st) {
-  using C = BrCfg<LOGN, S>;
-  const int64_t blocks = (B + C::CPB - 1) / C::CPB;
-  hipLaunchKernelGGL((blind_rotate_kernel<LOGN, S>), dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0,
-                     st, reinterpret_cast<const double2*>(ek->bk_fft), reinterpret_cast<const double2*>(ek->tw),
-                     ws.abar, testvec, ws.extract, ek->p.n, ek->p.l, ek->p.bg_bit, B);
-  return launch_status("blind_rotate_kernel");
+  constexpr int T = BrCfg<LOGN, S, 8>::T;
+  const int64_t cus = ek->cus > 0 ? ek->cus : 256;
+  auto fills = [&](int cpb) { return (B + cpb - 1) / cpb >= cus; };
+  if constexpr (T <= 64) {
+    if (fills(BrCfg<LOGN, S, 8>::CPB)) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
+    if (fills(BrCfg<LOGN, S, 4>::CPB)) return launch_br_blocks<LOGN, S, 4>(ek, ws, testvec, B, st);
+    if (fills(BrCfg<LOGN, S, 2>::CPB)) return launch_br_blocks<LOGN, S, 2>(ek, ws, testvec, B, st);
+    return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
+  } else if constexpr (T == 128) {
+    if (fills(BrCfg<LOGN, S, 8>::CPB)) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
+    return launch_br_blocks<LOGN, S, 2>(ek, ws, testvec, B, st);
+  } else {
+    return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
+  }
 }
 
 template <int LOGN, int S>
