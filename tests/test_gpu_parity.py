@@ -364,6 +364,38 @@ def test_tfhe128_nand_4096(torch):
     assert np.array_equal(got[idx], ref)
 
 
+def test_block_shapes_for_small_batches(torch):
+    """A batch too small to fill every CU with 8-wave blocks runs in blocks of
+    4, 2 or 1 waves (N = 1024) or of one ciphertext (N = 2048).  Every shape,
+    with a ragged last block, gives the same samples as the full batch, and
+    the last sample of each matches the oracle."""
+    for name, sizes in (("tfhe128_nand", (2100, 1024, 600, 200, 7)), ("lut3_n2048", (1102, 100))):
+        cfg = wl.CONFIGS[name]
+        p = cfg["params"]
+        sk, ek, ok = keys_for(name, torch)
+        if name == "tfhe128_nand":
+            a, b = wl.gate_inputs(cfg["input_seed"], cfg["batch"])
+            ca = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
+            cb = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), len(a))
+            run = lambda B: tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(
+                ek, "NAND", tfhe.to_device(ca[:B]), tfhe.to_device(cb[:B])))
+            ref_of = lambda idx: oracle.gate_bootstrap(ok, "NAND", ca[idx], cb[idx])
+        else:
+            m = wl.messages(cfg["input_seed"], cfg["batch"], cfg["msg_bits"])
+            tv = tfhe.tfhe_lut_testvec(p["N"], cfg["msg_bits"], wl.lut(cfg["input_seed"], cfg["msg_bits"]))
+            ct = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], (m << 28).astype(np.uint32))
+            run = lambda B: tfhe.to_host(tfhe.tfhe_lut_bootstrap_batch(ek, tfhe.to_device(ct[:B]), tfhe.to_device(tv)))
+            ref_of = lambda idx: oracle.lut_bootstrap(ok, ct[idx], tv)
+        say(f"block shapes {name} B={max(sizes)}")
+        full = run(max(sizes))
+        for B in sizes:
+            say(f"  B={B}")
+            assert np.array_equal(run(B), full[:B])
+        say("  oracle: last sample of each size")
+        idx = np.array([B - 1 for B in sizes])
+        assert np.array_equal(full[idx], ref_of(idx))
+
+
 def test_mlp_relu_7680(torch):
     cfg = wl.CONFIGS["mlp_relu"]
     p = cfg["params"]
