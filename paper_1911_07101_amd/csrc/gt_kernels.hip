@@ -1,11 +1,20 @@
 // HIP kernels of the TFHE activation path for gfx950 (MI355X).
 //
-//   prep_kernel          gate pre-combination (Section 3.1 gates; NOT is free)
-//                        and modulus switch of every LWE word to Z_{2N}
-//   blind_rotate_kernel  accumulator init, n CMux external products, SampleExtract
-//   keyswitch_kernel     LWE key switching back to dimension n
-//   relu_sign_kernel     trivial 0 for the sign bit of the ReLU output
-//   not_kernel           NOT without bootstrapping
+//   prep_kernel            gate pre-combination (Section 3.1 gates; NOT is free)
+//                          and modulus switch of every LWE word to Z_{2N}
+//   mux_combine_kernel     OR of a multiplexer's two exclusive halves
+//   lut_leaf_kernel        first multiplexer-tree level over constant leaves
+//   blind_rotate_kernel    accumulator init, n CMux external products,
+//                          SampleExtract; one wave per ciphertext (N <= 1024)
+//   blind_rotate_split_kernel  the same with two waves per ciphertext, each
+//                          computing one half of every transform (N = 2048)
+//   keyswitch_t8b2_kernel  LWE key switching back to dimension n (t = 8, base 4)
+//   keyswitch_kernel       the same for any other digit count and base
+//   relu_sign_kernel       trivial 0 for the sign bit of the ReLU output
+//   not_kernel             NOT without bootstrapping
+//   pack_init_kernel, pack_ks_kernel  functional key switching of LWE samples
+//                          into one ring sample
+//   sample_extract_kernel  LWE samples of chosen coefficients of ring samples
 //   negacyclic_mul_kernel  standalone ring product (checks the transform)
 //
 // The external product's negacyclic products are computed with a complex
@@ -14,15 +23,14 @@
 // transform's worst-case error stays below 1/8, so the rounded result equals
 // the exact product (bound in gt_host.cpp, transform_error_bound).
 //
-// Blind rotation layout: a ciphertext's transforms are held by T = N/8
-// threads with 4 complex points each (gt_layout.hpp): T = 128 (two waves) at
-// N = 1024, 256 at N = 2048.  The accumulator (two u32 polynomials), a
-// transpose scratch of N/2 complex points per ciphertext and a copy of the
-// twiddle table live in LDS; the transform-domain accumulators of an external
-// product ((mask, body) x key parts) live in registers.  The bootstrapping key
-// is read from global memory in the transform-domain layout, one 16-byte
-// point per load, coalesced across the T threads and shared by all
-// ciphertexts in flight through L2.
+// Blind rotation layout (gt_layout.hpp): a ciphertext's transforms are held
+// by N/16 lanes with 8 complex points each when the key has two parts: one
+// wave at N = 1024, two at N = 2048.  The accumulator (two u32 polynomials),
+// a transpose scratch per wave and copies of the twiddle tables live in LDS;
+// the transform-domain accumulators of an external product ((mask, body) x
+// key parts) live in registers.  The bootstrapping key is read from global
+// memory in the transform-domain layout, one 16-byte point per load,
+// coalesced across the wave and shared by the block's ciphertexts through L1.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -133,15 +141,19 @@ __device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* 
 // the same for every thread (tw_uniform, global memory, read through the
 // scalar cache), the others come from tw, an LDS copy laid out by
 // tw_lds_slot (TW_PERMUTED) or a natural-order table.
+// `tree` selects the tree whose pass-0 twiddles tw_uniform holds: 1 for a
+// transform of the whole tree, 2 + h for the subtree under node 2 + h of a
+// tree twice as large (its node m at the stage's level is node m + (1 + h)
+// times the level's first index there).
 template <class Lay, bool TW_PERMUTED, int p, int s, int g>
 __device__ __forceinline__ double2 twiddle(int t, const double2* __restrict__ tw,
-                                           const double2* __restrict__ tw_uniform) {
+                                           const double2* __restrict__ tw_uniform, int tree) {
   constexpr int N = Lay::N, LOGE = Lay::LOGE, E = Lay::E;
   constexpr int w = Lay::win(p);
   constexpr int b = s - w;
   constexpr int G = E >> (b + 1);
   if constexpr (p == 0)
-    return tw_uniform[(N >> (s + 1)) + g];
+    return tw_uniform[(N >> (s + 1)) * tree + g];
   else if constexpr (TW_PERMUTED)
     return tw[(N >> (s + 1)) + g * ((N >> (s + 1)) / G) + (t >> w)];
   else
@@ -165,7 +177,7 @@ __device__ __forceinline__ void ct_butterfly(double2& xe, double2& xe2, double2 
 template <class Lay, bool TW_PERMUTED>
 __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2* scr,
                                             const double2* __restrict__ tw,
-                                            const double2* __restrict__ tw_uniform) {
+                                            const double2* __restrict__ tw_uniform, int tree = 1) {
   constexpr int E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = decltype(PI)::value;
@@ -179,7 +191,7 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
       double2 z[G];
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
-        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform);
+        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform, tree);
       });
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
@@ -645,6 +657,213 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
   }
 }
 
+// ------------------------------------------ blind rotation, split transforms
+// Ring degree 2^LOGN whose transform spans two waves (T = 128 lanes).  The
+// forward transform's first stage splits C[X]/(X^n - i) into the halves
+// modulo X^{n/2} - tw[1] and X^{n/2} + tw[1]; wave h of a ciphertext computes
+// half h of every transform: that stage's output for its half, from input
+// points of both halves (read from the accumulator in LDS, which both waves
+// see), then the transform of the subtree under tree node 2 + h on its own,
+// with wave-local transposes.  The tree positions of half h are
+// n/2 * h + j', so the transform-domain layout (and the key) is the one of the
+// undivided transform.  The inverse transforms the halves separately; its
+// last stage combines them, for which the waves exchange their halves
+// through LDS one accumulator at a time.  A CMux then takes 2O block
+// barriers instead of two per transpose.
+template <int LOGN, int S, int WPB>
+struct BrSplitCfg {
+  using Lay = RingLayout<LOGN, S>;
+  using Sub = Layout<Lay::LOGN - 1, Lay::LOGE>;
+  static_assert(Lay::T == 128 && Sub::T == 64, "two waves per ciphertext");
+  static constexpr int NR = 1 << LOGN, NC = Lay::N, HN = Sub::N, E = Sub::E;
+  static constexpr int O = 2 * S;
+  static constexpr int SHIFT = S == 2 ? 16 : 11;
+  static constexpr int CPB = WPB / 2;
+  static constexpr int THREADS = CPB * 128;
+  static constexpr int LDS_BYTES = 2 * HN * 16 + CPB * 2 * Sub::SCR * 16 + CPB * 2 * NR * 4;
+  static_assert(CPB >= 1 && LDS_BYTES <= 160 * 1024, "block exceeds the CU's LDS");
+  static constexpr int MIN_WAVES = 2;
+};
+
+template <int LOGN, int S, int WPB>
+__global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
+                             (BrSplitCfg<LOGN, S, WPB>::MIN_WAVES)) void blind_rotate_split_kernel(
+    const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
+    const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
+    int64_t B) {
+  using C = BrSplitCfg<LOGN, S, WPB>;
+  using Sub = typename C::Sub;
+  constexpr int NR = C::NR, NC = C::NC, HN = C::HN, E = C::E, CPB = C::CPB, O = C::O;
+  constexpr int TOP = C::Lay::LOGN - 1;  // the splitting stage
+  __shared__ double2 s_tw[2 * HN];
+  __shared__ double2 s_scr[CPB * 2 * Sub::SCR];
+  __shared__ uint32_t s_acc[CPB * 2 * NR];
+
+  const int slot = threadIdx.x / 128;
+  const int tc = threadIdx.x % 128;  // thread within the ciphertext
+  const int h = __builtin_amdgcn_readfirstlane(tc >> 6);  // the half this wave computes
+  const int t = tc & 63;
+  int64_t c = static_cast<int64_t>(blockIdx.x) * CPB + slot;
+  const bool active = c < B;
+  if (!active) c = B - 1;  // idle slots repeat the last sample and write nothing
+
+  // subtree tables: node m of the subtree under node 2 + hh is tree node
+  // m + (1 + hh) 2^floor(log2 m); each stored in the subtree's LDS order
+  for (int k = threadIdx.x; k < 2 * HN; k += C::THREADS) {
+    const int hh = k / HN, m = k % HN;
+    const int top = m > 0 ? 1 << (31 - __builtin_clz(static_cast<unsigned>(m))) : 0;
+    s_tw[hh * HN + tw_lds_slot<Sub>(m)] = tw_g[m + (1 + hh) * top];
+  }
+  double2* scr = s_scr + (slot * 2 + h) * Sub::SCR;
+  const double2* partner = s_scr + (slot * 2 + (1 - h)) * Sub::SCR;
+  const double2* tw_half = s_tw + h * HN;
+  uint32_t* acc_a = s_acc + slot * 2 * NR;
+  uint32_t* acc_b = acc_a + NR;
+  const uint16_t* ab = abar + c * (n + 1);
+  const BufTable itw{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + NC), 0, NC * 16, 0x00020000)};
+  const BufTable twist{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + 2 * NC), 0, NC * 16, 0x00020000)};
+  const double2 tw1 = tw_g[1];
+  const double2 split_w = h ? make_double2(-tw1.x, -tw1.y) : tw1;
+
+  // ACC = (0, X^{-bbar} v)
+  {
+    const uint32_t bbar = ab[n];
+    const uint32_t e0 = (2u * NR - bbar) & (2u * NR - 1);
+    for (int j = tc; j < NR; j += 128) {
+      uint32_t v;
+      if (testvec == nullptr) {
+        const int src = j - static_cast<int>(e0 & (NR - 1));
+        const uint32_t m = static_cast<uint32_t>(src >> 31) ^ (0u - ((e0 / NR) & 1u));
+        v = (kMu ^ m) - m;
+      } else {
+        v = rot_coef<NR>(testvec, e0, j);
+      }
+      acc_a[j] = 0u;
+      acc_b[j] = v;
+    }
+  }
+  __syncthreads();
+
+  const uint32_t half = 1u << (bg_bit - 1);
+  uint32_t offset = 0, flip = 0;
+  for (int j = 1; j <= l; j++) {
+    offset += half << (32 - j * bg_bit);
+    flip |= half << (32 - j * bg_bit);
+  }
+  if (l * bg_bit < 32) offset += 1u << (31 - l * bg_bit);
+  const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;
+  const uint32_t voff = static_cast<uint32_t>(tc) * 16u;
+
+  for (int i = 0; i < n; i++) {
+    const uint32_t a_i = ab[i];
+    const __amdgpu_buffer_rsrc_t bkr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
+                                          static_cast<int>(bk_step * 16), 0x00020000);
+    double2 acc[O][E];
+#pragma unroll
+    for (int o = 0; o < O; o++)
+#pragma unroll
+      for (int e = 0; e < E; e++) acc[o][e] = make_double2(0.0, 0.0);
+
+    for (int q = 0; q < 2; q++) {
+      const uint32_t* P = q ? acc_b : acc_a;
+      for (int jj = 0; jj < l; jj++) {
+        const uint32_t lsh = static_cast<uint32_t>(jj * bg_bit), rsh = static_cast<uint32_t>(32 - bg_bit);
+        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
+        double2 w[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>(e * 128 * 16));
+        // digit jj of D = X^{a_i} P - P (plus the decomposition offset),
+        // recomputed from LDS for each digit (holding D for both halves would
+        // take 4E registers): point j' + n/2 * hh of the subtree points
+        // j' = t + 64 e is coefficients j' + n/2 * hh (real part) and
+        // j' + n/2 * hh + n (imaginary part).  Then the splitting stage: this
+        // half's output u + w v (half 0) or u - w v (half 1).
+        uint32_t a_q = a_i;
+        int t_q = t;
+        asm volatile("" : "+v"(a_q), "+v"(t_q));
+        double2 x[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) {
+          double dg[2][2];
+#pragma unroll
+          for (int hh = 0; hh < 2; hh++)
+#pragma unroll
+            for (int im = 0; im < 2; im++) {
+              const int j = t_q + 64 * e + hh * HN + im * NC;
+              const uint32_t D = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
+              dg[hh][im] = static_cast<double>(static_cast<int32_t>(D << lsh) >> rsh);
+            }
+          const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
+          x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
+                              fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+        }
+        fft_forward<Sub, true>(x, t, scr, tw_half, tw_g, 2 + h);
+#pragma unroll
+        for (int o = 0; o < O; o++) {
+          if (o > 0) {
+#pragma unroll
+            for (int e = 0; e < E; e++)
+              w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>((o * E + e) * 128 * 16));
+          }
+#pragma unroll
+          for (int e = 0; e < E; e++) cmac(acc[o][e], x[e], w[e]);
+        }
+      }
+    }
+
+    // inverse transforms of this half, two at a time
+    static_for<0, O / 2>([&](auto PI) { fft_inverse<Sub, 2 * decltype(PI)::value, 2>(acc, t, scr, itw); });
+    // the inverse's last stage: point j' of half 0 becomes u + t_j' v, of
+    // half 1 u - t_j' v (u, v: the halves' values at j', t_j' = e^{-2 pi i j'/n})
+    int t_x = t;
+    asm volatile("" : "+v"(t_x));
+    static_for<0, O>([&](auto OI) {
+      constexpr int o = decltype(OI)::value;
+      if constexpr (o > 0) __syncthreads();  // the partner has read the previous accumulator
+#pragma unroll
+      for (int e = 0; e < E; e++) scr[t_x + 64 * e] = acc[o][e];
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < E; e++) {
+        const double2 pv = partner[t_x + 64 * e];
+        const double2 tk = itw(t_x, (1 << TOP) - 1 + 64 * e);
+        const double2 a = h ? pv : acc[o][e], b = h ? acc[o][e] : pv;
+        const double2 ts = h ? make_double2(-tk.x, -tk.y) : tk;
+        acc[o][e] = make_double2(fma(ts.x, b.x, fma(-ts.y, b.y, a.x)), fma(ts.x, b.y, fma(ts.y, b.x, a.y)));
+      }
+    });
+    // twist, round (every output is within 1/8 of an integer), recombine the
+    // key parts and add to this half's coefficients
+#pragma unroll
+    for (int e = 0; e < E; e++) {
+      const int j = t_x + 64 * e + h * HN;
+      const double2 tau = twist(t_x, 64 * e + h * HN);
+      uint32_t ra0 = 0u, ra1 = 0u, rb0 = 0u, rb1 = 0u;
+#pragma unroll
+      for (int sp = S - 1; sp >= 0; sp--) {
+        const double2 va = cmul(acc[sp][e], tau), vb = cmul(acc[S + sp][e], tau);
+        ra0 = (ra0 << C::SHIFT) + round_low32(va.x);
+        ra1 = (ra1 << C::SHIFT) + round_low32(va.y);
+        rb0 = (rb0 << C::SHIFT) + round_low32(vb.x);
+        rb1 = (rb1 << C::SHIFT) + round_low32(vb.y);
+      }
+      acc_a[j] += ra0;
+      acc_a[j + NC] += ra1;
+      acc_b[j] += rb0;
+      acc_b[j + NC] += rb1;
+    }
+    __syncthreads();
+  }
+
+  // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0)
+  if (active) {
+    uint32_t* out = extract + c * (NR + 1);
+    for (int j = tc; j < NR; j += 128) out[j] = j == 0 ? acc_a[0] : 0u - acc_a[NR - j];
+    if (tc == 0) out[NR] = acc_b[0];
+  }
+}
+
 // ------------------------------------------------------- key switching
 // Output sample of batch entry c: c itself, or for the activation units the
 // gate's place in the [V][bits] output tensor (forward ReLU: bit
@@ -1036,6 +1255,18 @@ int launch_br_blocks(const tfhe_eval_key* ek, const Workspace& ws, const uint32_
   return launch_status("blind_rotate_kernel");
 }
 
+template <int LOGN, int S, int WPB>
+int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
+                    hipStream_t st) {
+  using C = BrSplitCfg<LOGN, S, WPB>;
+  const int64_t blocks = (B + C::CPB - 1) / C::CPB;
+  hipLaunchKernelGGL((blind_rotate_split_kernel<LOGN, S, WPB>), dim3(static_cast<unsigned>(blocks)),
+                     dim3(C::THREADS), 0, st, reinterpret_cast<const double2*>(ek->bk_fft),
+                     reinterpret_cast<const double2*>(ek->tw), ws.abar, testvec, ws.extract, ek->p.n, ek->p.l,
+                     ek->p.bg_bit, B);
+  return launch_status("blind_rotate_split_kernel");
+}
+
 // Blocks of 8 waves when the batch fills every CU with one (or more), else
 // the largest of 4, 2, 1 waves per block that still gives every CU a block:
 // a small batch then runs one or two waves per SIMD, where its CMux chain is
@@ -1053,8 +1284,8 @@ int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* test
     if (fills(BrCfg<LOGN, S, 2>::CPB)) return launch_br_blocks<LOGN, S, 2>(ek, ws, testvec, B, st);
     return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
   } else if constexpr (T == 128) {
-    if (fills(BrCfg<LOGN, S, 8>::CPB)) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
-    return launch_br_blocks<LOGN, S, 2>(ek, ws, testvec, B, st);
+    if (fills(BrSplitCfg<LOGN, S, 8>::CPB)) return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
+    return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
   } else {
     return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
   }
