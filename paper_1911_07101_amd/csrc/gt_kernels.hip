@@ -668,7 +668,7 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
 // n/2 * h + j', so the transform-domain layout (and the key) is the one of the
 // undivided transform.  The inverse transforms the halves separately; its
 // last stage combines them, for which the waves exchange their halves
-// through LDS one accumulator at a time.  A CMux then takes 2O block
+// through LDS one accumulator at a time.  A CMux then takes O + 1 block
 // barriers instead of two per transpose.
 template <int LOGN, int S, int WPB>
 struct BrSplitCfg {
@@ -715,7 +715,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     s_tw[hh * HN + tw_lds_slot<Sub>(m)] = tw_g[m + (1 + hh) * top];
   }
   double2* scr = s_scr + (slot * 2 + h) * Sub::SCR;
-  const double2* partner = s_scr + (slot * 2 + (1 - h)) * Sub::SCR;
+  double2* partner = s_scr + (slot * 2 + (1 - h)) * Sub::SCR;
   const double2* tw_half = s_tw + h * HN;
   uint32_t* acc_a = s_acc + slot * 2 * NR;
   uint32_t* acc_b = acc_a + NR;
@@ -818,15 +818,20 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     // half 1 u - t_j' v (u, v: the halves' values at j', t_j' = e^{-2 pi i j'/n})
     int t_x = t;
     asm volatile("" : "+v"(t_x));
+    // Accumulator o goes through the writer's own scratch when o is even and
+    // through the partner's when o is odd: a wave overwrites a region only
+    // after it has itself read what was last written there, so one barrier
+    // per accumulator suffices.
     static_for<0, O>([&](auto OI) {
       constexpr int o = decltype(OI)::value;
-      if constexpr (o > 0) __syncthreads();  // the partner has read the previous accumulator
+      double2* dst = (o & 1) ? partner : scr;
+      const double2* src = (o & 1) ? scr : partner;
 #pragma unroll
-      for (int e = 0; e < E; e++) scr[t_x + 64 * e] = acc[o][e];
+      for (int e = 0; e < E; e++) dst[t_x + 64 * e] = acc[o][e];
       __syncthreads();
 #pragma unroll
       for (int e = 0; e < E; e++) {
-        const double2 pv = partner[t_x + 64 * e];
+        const double2 pv = src[t_x + 64 * e];
         const double2 tk = itw(t_x, (1 << TOP) - 1 + 64 * e);
         const double2 a = h ? pv : acc[o][e], b = h ? acc[o][e] : pv;
         const double2 ts = h ? make_double2(-tk.x, -tk.y) : tk;
