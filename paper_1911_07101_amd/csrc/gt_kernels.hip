@@ -160,6 +160,16 @@ __device__ __forceinline__ double2 twiddle(int t, const double2* __restrict__ tw
     return tw[(N >> (s + 1)) + ((t >> w) << (LOGE - b - 1)) + g];
 }
 
+// signed bit field [pos, pos + width) of x, 0 < width < 32, in one
+// instruction.  Written as inline assembly: the compiler's own bit-field
+// intrinsic has been seen followed by an unsigned int-to-double conversion
+// here, which would turn negative digits positive.
+__device__ __forceinline__ int32_t signed_field(uint32_t x, uint32_t pos, uint32_t width) {
+  int32_t r;
+  asm("v_bfe_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "s"(pos), "v"(width));
+  return r;
+}
+
 // Cooley-Tukey butterfly (xe, xe2) <- (u + w v, u - w v): a = u + w v in four
 // FMAs, b = 2u - a in two
 __device__ __forceinline__ void ct_butterfly(double2& xe, double2& xe2, double2 w) {
@@ -584,9 +594,9 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
           D[h][e] = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
         }
       for (int jj = 0; jj < l; jj++) {
-        // digit jj sits in bits [32 - (jj+1) bg_bit, 32 - jj bg_bit): move it
-        // to the top, then shift it down arithmetically (sign extension)
-        const uint32_t lsh = static_cast<uint32_t>(jj * bg_bit), rsh = static_cast<uint32_t>(32 - bg_bit);
+        // digit jj is the signed field of bits [32 - (jj+1) bg_bit, 32 - jj bg_bit)
+        // (bg_bit < 32: the transform bound admits no wider digit)
+        const uint32_t dpos = static_cast<uint32_t>(32 - (jj + 1) * bg_bit), dw = static_cast<uint32_t>(bg_bit);
         // key row r = q*l + jj; its first output's points are requested
         // before the transform so that their latency overlaps it
         const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
@@ -596,8 +606,8 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
         double2 x[E];
 #pragma unroll
         for (int e = 0; e < E; e++)
-          x[e] = make_double2(static_cast<double>(static_cast<int32_t>(D[0][e] << lsh) >> rsh),
-                              static_cast<double>(static_cast<int32_t>(D[1][e] << lsh) >> rsh));
+          x[e] = make_double2(static_cast<double>(signed_field(D[0][e], dpos, dw)),
+                              static_cast<double>(signed_field(D[1][e], dpos, dw)));
         fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
         if constexpr (kCmuxBarrier)
           if (late_barrier && first_forward) __syncthreads();
@@ -768,7 +778,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
       for (int jj = 0; jj < l; jj++) {
-        const uint32_t lsh = static_cast<uint32_t>(jj * bg_bit), rsh = static_cast<uint32_t>(32 - bg_bit);
+        const uint32_t dpos = static_cast<uint32_t>(32 - (jj + 1) * bg_bit), dw = static_cast<uint32_t>(bg_bit);
         const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
         double2 w[E];
 #pragma unroll
@@ -792,7 +802,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
             for (int im = 0; im < 2; im++) {
               const int j = t_q + 64 * e + hh * HN + im * NC;
               const uint32_t D = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
-              dg[hh][im] = static_cast<double>(static_cast<int32_t>(D << lsh) >> rsh);
+              dg[hh][im] = static_cast<double>(signed_field(D, dpos, dw));
             }
           const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
           x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
