@@ -193,22 +193,38 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
     constexpr int p = decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
+    // the first stage's twiddles are requested before the pass's transpose and
+    // the other stages' right after it, so that their round trips overlap the
+    // transpose and the first stage instead of following each other.  A
+    // thread's twiddles g and g + 1 (g even) belong to sibling tree nodes 2k
+    // and 2k + 1, whose twiddles differ by the factor zeta^{N/2} = i: only
+    // the even ones are read, the odd ones are i times them (exact: a swap
+    // and a sign, which the butterflies' FMAs take as source modifiers)
+    double2 z[NS][E / 2];
+    auto fetch = [&](auto SI) {
+      constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
+      constexpr int G = E >> (s - w + 1);
+      static_for<0, G>([&](auto GI) {
+        constexpr int g = decltype(GI)::value;
+        if constexpr ((g & 1) == 0)
+          z[decltype(SI)::value][g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform, tree);
+        else
+          z[decltype(SI)::value][g] = make_double2(-z[decltype(SI)::value][g - 1].y, z[decltype(SI)::value][g - 1].x);
+      });
+    };
+    fetch(std::integral_constant<int, 0>{});
     if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w>(x, t, scr);
+    static_for<1, NS>(fetch);
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
       constexpr int b = s - w;
       constexpr int G = E >> (b + 1);
-      double2 z[G];
-      static_for<0, G>([&](auto GI) {
-        constexpr int g = decltype(GI)::value;
-        z[g] = twiddle<Lay, TW_PERMUTED, p, s, g>(t, tw, tw_uniform, tree);
-      });
       static_for<0, G>([&](auto GI) {
         constexpr int g = decltype(GI)::value;
         static_for<0, (1 << b)>([&](auto LI) {
           constexpr int e = (g << (b + 1)) | decltype(LI)::value;
           constexpr int e2 = e | (1 << b);
-          ct_butterfly(x[e], x[e2], z[g]);
+          ct_butterfly(x[e], x[e2], z[decltype(SI)::value][g]);
         });
       });
     });
@@ -254,6 +270,26 @@ __device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, doub
     constexpr int p = Lay::NPASS - 1 - decltype(PI)::value;
     constexpr int w = Lay::win(p);
     constexpr int NS = Lay::hi(p) - Lay::lo(p);
+    // stage twiddles of the pass (none in the pass whose window starts at bit
+    // 0: constants there), requested before its transposes.  Twiddle g + NG/2
+    // of a stage (NG = 2^b per thread) has the angle index c + 2^(s-1) of
+    // twiddle g, so it is -i times it: only the first half is read
+    double2 zp[NS][E / 2];
+    if constexpr (w != 0) {
+      const int lane = t & ((1 << w) - 1);
+      static_for<0, NS>([&](auto SI) {
+        constexpr int s = Lay::lo(p) + decltype(SI)::value;
+        constexpr int NG = 1 << (s - w);
+        static_for<0, NG>([&](auto GI) {
+          constexpr int g = decltype(GI)::value;
+          if constexpr (NG == 1 || g < NG / 2)
+            zp[decltype(SI)::value][g] = itw(lane, (1 << s) - 1 + (g << w));
+          else
+            zp[decltype(SI)::value][g] =
+                make_double2(zp[decltype(SI)::value][g - NG / 2].y, -zp[decltype(SI)::value][g - NG / 2].x);
+        });
+      });
+    }
     if constexpr (p < Lay::NPASS - 1)
       static_for<K0, K0 + K>([&](auto KI) { transpose<Lay, Lay::win(p + 1), w>(x[decltype(KI)::value], t, scr); });
     static_for<0, NS>([&](auto SI) {
@@ -270,17 +306,11 @@ __device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, doub
         });
       } else {
         // position j mod 2^s = (t mod 2^w) | ((e mod 2^b) << w)
-        double2 z[NG];
-        const int lane = t & ((1 << w) - 1);
-        static_for<0, NG>([&](auto GI) {
-          constexpr int g = decltype(GI)::value;
-          z[g] = itw(lane, (1 << s) - 1 + (g << w));
-        });
         static_for<K0, K0 + K>([&](auto KI) {
           constexpr int k = decltype(KI)::value;
           static_for<0, E>([&](auto EI) {
             constexpr int e = decltype(EI)::value;
-            if constexpr ((e & NG) == 0) ct_butterfly(x[k][e], x[k][e | NG], z[e & (NG - 1)]);
+            if constexpr ((e & NG) == 0) ct_butterfly(x[k][e], x[k][e | NG], zp[decltype(SI)::value][e & (NG - 1)]);
           });
         });
       }
