@@ -456,6 +456,11 @@ def main():
         "transform": {"key_parts": parts, "worst_case_error": bound},
         "kernel_source_digest": digest,
         "device": torch.cuda.get_device_name(0),
+        # the paper's CPU timing of the same activation path (its own TFHE
+        # parameters and hardware): context, not a baseline for this metric
+        "paper_context": {"relu_unit_s": 0.1, "softmax_unit_s": 3.3, "bootstraps_per_relu_unit": 7,
+                          "hardware": "Intel Xeon E7-8890 v4, 2.2 GHz, 2 sockets x 12 cores, single-core runs",
+                          "source": "Section 3.1 (forward/backward ReLU, forward softmax), Section 4 setup"},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, ca_h, cb_h, out)

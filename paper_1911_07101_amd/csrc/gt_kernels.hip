@@ -114,11 +114,15 @@ __host__ __device__ constexpr int tw_lds_slot(int k) {
   return start + (m % G) * rows + m / G;
 }
 
-template <class Lay, int WFROM, int WTO>
+template <class Lay, int WFROM, int WTO, bool PRIO>
 __device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* scr) {
   // one base address per layout where the slots are affine in e (immediate offsets)
   double2* wr = scr + Lay::slot(Lay::jmap(t, 0, WFROM));
   double2* rd = scr + Lay::slot(Lay::jmap(t, 0, WTO));
+  // PRIO: the wave's instruction-issue priority is raised while it issues
+  // the transpose's LDS operations, so that they are queued before the other
+  // waves' arithmetic and their latency overlaps it
+  if constexpr (PRIO) __builtin_amdgcn_s_setprio(3);
   static_for<0, Lay::E>([&](auto EI) {
     constexpr int e = decltype(EI)::value;
     if constexpr (Lay::affine(WFROM))
@@ -134,6 +138,7 @@ __device__ __forceinline__ void transpose(double2 (&x)[Lay::E], int t, double2* 
     else
       x[e] = scr[Lay::slot(Lay::jmap(t, e, WTO))];
   });
+  if constexpr (PRIO) __builtin_amdgcn_s_setprio(0);
   poly_sync<Lay::T>();
 }
 
@@ -184,7 +189,7 @@ __device__ __forceinline__ void ct_butterfly(double2& xe, double2& xe2, double2 
 // k = n/2^(s+1) + j/2^(s+1) and multiplies by tw[k]).  In: pass-0 (coefficient)
 // layout; out: last-pass (transform) layout.  Each stage fetches its own
 // twiddles (one per butterfly group of the thread).
-template <class Lay, bool TW_PERMUTED>
+template <class Lay, bool TW_PERMUTED, bool PRIO = false>
 __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2* scr,
                                             const double2* __restrict__ tw,
                                             const double2* __restrict__ tw_uniform, int tree = 1) {
@@ -213,7 +218,7 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
       });
     };
     fetch(std::integral_constant<int, 0>{});
-    if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w>(x, t, scr);
+    if constexpr (p > 0) transpose<Lay, Lay::win(p - 1), w, PRIO>(x, t, scr);
     static_for<1, NS>(fetch);
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::hi(p) - 1 - decltype(SI)::value;
@@ -262,7 +267,7 @@ __device__ __forceinline__ void dit_const_butterfly(double2& xe, double2& xe2) {
 // of the index, constant part); the polynomials share them, and one
 // polynomial's transpose is in flight while another's butterflies run.
 // In: transform layout; out: coefficient layout.
-template <class Lay, int K0, int K, int M, class Tab>
+template <class Lay, int K0, int K, bool PRIO = false, int M, class Tab>
 __device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, double2* scr, const Tab& itw) {
   static_assert(K0 + K <= M, "polynomial range");
   constexpr int E = Lay::E;
@@ -291,7 +296,7 @@ __device__ __forceinline__ void fft_inverse(double2 (&x)[M][Lay::E], int t, doub
       });
     }
     if constexpr (p < Lay::NPASS - 1)
-      static_for<K0, K0 + K>([&](auto KI) { transpose<Lay, Lay::win(p + 1), w>(x[decltype(KI)::value], t, scr); });
+      static_for<K0, K0 + K>([&](auto KI) { transpose<Lay, Lay::win(p + 1), w, PRIO>(x[decltype(KI)::value], t, scr); });
     static_for<0, NS>([&](auto SI) {
       constexpr int s = Lay::lo(p) + decltype(SI)::value;
       constexpr int b = s - w;
@@ -584,17 +589,10 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
 
   // One block barrier per CMux keeps the block's ciphertexts on the same
   // CMux: they then read the same key points close together in time, which
-  // the L1 cache serves.  The upper half of the block's waves takes it after
-  // its first forward transform instead of at the start of the CMux, so the
-  // two waves sharing a SIMD (waves w and w + 4) run one transform apart and
-  // one's butterflies overlap the other's LDS waits.  Every wave passes one
-  // barrier per CMux (there are 2l >= 2 forward transforms per CMux).
+  // the L1 cache serves.
   constexpr bool kCmuxBarrier = CPB > 1 && T <= 64;
-  const bool late_barrier = kCmuxBarrier && CPB * T == 512 && (__builtin_amdgcn_readfirstlane(threadIdx.x) >> 8) != 0;
   for (int i = 0; i < n; i++) {
-    if constexpr (kCmuxBarrier)
-      if (!late_barrier) __syncthreads();
-    bool first_forward = true;
+    if constexpr (kCmuxBarrier) __syncthreads();
     const uint32_t a_i = ab[i];
     const __amdgpu_buffer_rsrc_t bkr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
@@ -639,9 +637,6 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
           x[e] = make_double2(static_cast<double>(signed_field(D[0][e], dpos, dw)),
                               static_cast<double>(signed_field(D[1][e], dpos, dw)));
         fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
-        if constexpr (kCmuxBarrier)
-          if (late_barrier && first_forward) __syncthreads();
-        first_forward = false;
 #pragma unroll
         for (int o = 0; o < O; o++) {
           if (o > 0) {
@@ -823,6 +818,10 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
         int t_q = t;
         asm volatile("" : "+v"(a_q), "+v"(t_q));
         double2 x[E];
+        // raised issue priority while the digits' LDS reads are issued (as
+        // in the transposes): measured 7 % faster at N = 2048, where the
+        // two waves of a ciphertext wait on each other at the block barriers
+        __builtin_amdgcn_s_setprio(3);
 #pragma unroll
         for (int e = 0; e < E; e++) {
           double dg[2][2];
@@ -838,7 +837,8 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
           x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
                               fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
         }
-        fft_forward<Sub, true>(x, t, scr, tw_half, tw_g, 2 + h);
+        __builtin_amdgcn_s_setprio(0);
+        fft_forward<Sub, true, true>(x, t, scr, tw_half, tw_g, 2 + h);
 #pragma unroll
         for (int o = 0; o < O; o++) {
           if (o > 0) {
@@ -853,7 +853,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     }
 
     // inverse transforms of this half, two at a time
-    static_for<0, O / 2>([&](auto PI) { fft_inverse<Sub, 2 * decltype(PI)::value, 2>(acc, t, scr, itw); });
+    static_for<0, O / 2>([&](auto PI) { fft_inverse<Sub, 2 * decltype(PI)::value, 2, true>(acc, t, scr, itw); });
     // the inverse's last stage: point j' of half 0 becomes u + t_j' v, of
     // half 1 u - t_j' v (u, v: the halves' values at j', t_j' = e^{-2 pi i j'/n})
     int t_x = t;
