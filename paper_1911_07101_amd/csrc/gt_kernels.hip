@@ -702,9 +702,10 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
 // with wave-local transposes.  The tree positions of half h are
 // n/2 * h + j', so the transform-domain layout (and the key) is the one of the
 // undivided transform.  The inverse transforms the halves separately; its
-// last stage combines them, for which the waves exchange their halves
-// through LDS one accumulator at a time.  A CMux then takes O + 1 block
-// barriers instead of two per transpose.
+// last stage combines them: each wave finishes both halves for half of the
+// points, exchanging the other half of its points with its partner through
+// LDS two accumulators at a time.  A CMux then takes O/2 + 1 block barriers
+// instead of two per transpose.
 template <int LOGN, int S, int WPB>
 struct BrSplitCfg {
   using Lay = RingLayout<LOGN, S>;
@@ -855,48 +856,86 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     // inverse transforms of this half, two at a time
     static_for<0, O / 2>([&](auto PI) { fft_inverse<Sub, 2 * decltype(PI)::value, 2, true>(acc, t, scr, itw); });
     // the inverse's last stage: point j' of half 0 becomes u + t_j' v, of
-    // half 1 u - t_j' v (u, v: the halves' values at j', t_j' = e^{-2 pi i j'/n})
+    // half 1 u - t_j' v (u, v: the halves' values at j', t_j' = e^{-2 pi i j'/n}).
+    // Wave h finishes both halves for its slice of the points j' = t + 64 e,
+    // e in [h E/2, h E/2 + E/2): it sends the other slice of its half to the
+    // partner and receives the partner's values at its own slice.  Two
+    // accumulators at a time go through LDS (E points per lane), the first
+    // pair through the writer's own scratch, the second through the
+    // partner's: a wave overwrites a region only after it has itself read
+    // what was last written there, so one barrier per pair suffices.
     int t_x = t;
     asm volatile("" : "+v"(t_x));
-    // Accumulator o goes through the writer's own scratch when o is even and
-    // through the partner's when o is odd: a wave overwrites a region only
-    // after it has itself read what was last written there, so one barrier
-    // per accumulator suffices.
-    static_for<0, O>([&](auto OI) {
-      constexpr int o = decltype(OI)::value;
-      double2* dst = (o & 1) ? partner : scr;
-      const double2* src = (o & 1) ? scr : partner;
+    auto finish = [&](auto HI) {
+      constexpr int H = decltype(HI)::value, HE = E / 2;
+      constexpr int MINE = H * HE, OTHER = (1 - H) * HE;
+      double2 tk[HE];  // the stage's twiddles at this slice, the same for every accumulator
 #pragma unroll
-      for (int e = 0; e < E; e++) dst[t_x + 64 * e] = acc[o][e];
-      __syncthreads();
+      for (int e = 0; e < HE; e++) tk[e] = itw(t_x, (1 << TOP) - 1 + 64 * (MINE + e));
+      // twist, round (every output is within 1/8 of an integer), recombine
+      // the key parts of polynomial q and add to both halves' coefficients
+      // at this slice
+      auto accumulate = [&](auto QI) {
+        constexpr int q = decltype(QI)::value;
+        uint32_t* dstp = q ? acc_b : acc_a;
 #pragma unroll
-      for (int e = 0; e < E; e++) {
-        const double2 pv = src[t_x + 64 * e];
-        const double2 tk = itw(t_x, (1 << TOP) - 1 + 64 * e);
-        const double2 a = h ? pv : acc[o][e], b = h ? acc[o][e] : pv;
-        const double2 ts = h ? make_double2(-tk.x, -tk.y) : tk;
-        acc[o][e] = make_double2(fma(ts.x, b.x, fma(-ts.y, b.y, a.x)), fma(ts.x, b.y, fma(ts.y, b.x, a.y)));
+        for (int e = 0; e < HE; e++)
+#pragma unroll
+          for (int hh = 0; hh < 2; hh++) {
+            const int slot_e = hh ? OTHER + e : MINE + e;
+            const int j = t_x + 64 * (MINE + e) + hh * HN;
+            const double2 tau = twist(t_x, 64 * (MINE + e) + hh * HN);
+            uint32_t r0 = 0u, r1 = 0u;
+#pragma unroll
+            for (int sp = S - 1; sp >= 0; sp--) {
+              const double2 v = cmul(acc[q * S + sp][slot_e], tau);
+              r0 = (r0 << C::SHIFT) + round_low32(v.x);
+              r1 = (r1 << C::SHIFT) + round_low32(v.y);
+            }
+            dstp[j] += r0;
+            dstp[j + NC] += r1;
+          }
+      };
+      static_for<0, O / 2>([&](auto KI) {
+        constexpr int k = decltype(KI)::value;
+        double2* dst = (k & 1) ? partner : scr;
+        const double2* src = (k & 1) ? scr : partner;
+        static_for<0, 2>([&](auto PI) {
+          constexpr int pi = decltype(PI)::value;
+#pragma unroll
+          for (int e = 0; e < HE; e++) dst[(pi * HE + e) * 64 + t_x] = acc[2 * k + pi][OTHER + e];
+        });
+        __syncthreads();
+        static_for<0, 2>([&](auto PI) {
+          constexpr int pi = decltype(PI)::value, o = 2 * k + pi;
+#pragma unroll
+          for (int e = 0; e < HE; e++) {
+            const double2 pv = src[(pi * HE + e) * 64 + t_x];
+            double2 u = H ? pv : acc[o][MINE + e], v = H ? acc[o][MINE + e] : pv;
+            ct_butterfly(u, v, tk[e]);
+            acc[o][MINE + e] = u;   // half 0's point j'
+            acc[o][OTHER + e] = v;  // half 1's point j'
+          }
+        });
+        // with two key parts the first pair is the mask's, the second the body's
+        if constexpr (S == 2) accumulate(std::integral_constant<int, k>{});
+      });
+      if constexpr (S != 2) {
+        accumulate(std::integral_constant<int, 0>{});
+        accumulate(std::integral_constant<int, 1>{});
       }
-    });
-    // twist, round (every output is within 1/8 of an integer), recombine the
-    // key parts and add to this half's coefficients
-#pragma unroll
-    for (int e = 0; e < E; e++) {
-      const int j = t_x + 64 * e + h * HN;
-      const double2 tau = twist(t_x, 64 * e + h * HN);
-      uint32_t ra0 = 0u, ra1 = 0u, rb0 = 0u, rb1 = 0u;
-#pragma unroll
-      for (int sp = S - 1; sp >= 0; sp--) {
-        const double2 va = cmul(acc[sp][e], tau), vb = cmul(acc[S + sp][e], tau);
-        ra0 = (ra0 << C::SHIFT) + round_low32(va.x);
-        ra1 = (ra1 << C::SHIFT) + round_low32(va.y);
-        rb0 = (rb0 << C::SHIFT) + round_low32(vb.x);
-        rb1 = (rb1 << C::SHIFT) + round_low32(vb.y);
-      }
-      acc_a[j] += ra0;
-      acc_a[j + NC] += ra1;
-      acc_b[j] += rb0;
-      acc_b[j + NC] += rb1;
+    };
+    // two copies, one per half; the distinct empty asm statements keep the
+    // compiler from merging them into one path that selects between the
+    // register slices (which would hold both slices' values at once)
+    if (h == 0) {
+      asm volatile("; last stage, half 0");
+      finish(std::integral_constant<int, 0>{});
+      asm volatile("; last stage, half 0 done");
+    } else {
+      asm volatile("; last stage, half 1");
+      finish(std::integral_constant<int, 1>{});
+      asm volatile("; last stage, half 1 done");
     }
     __syncthreads();
   }

@@ -130,6 +130,35 @@ def test_blind_rotate_extract_parity_toy(torch):
     assert np.array_equal(got, oracle.bootstrap_no_ks(ok, x, tv))
 
 
+# parameter sets whose transform bound needs the key in three parts: the
+# three-part blind-rotation kernels (4 points per lane) at every ring size
+THREE_PARTS = {
+    256: dict(n=8, N=256, l=1, bg_bit=18, ks_t=8, ks_basebit=2, alpha_lwe=2**-15, alpha_bk=2**-25),
+    512: dict(n=8, N=512, l=1, bg_bit=16, ks_t=8, ks_basebit=2, alpha_lwe=2**-15, alpha_bk=2**-25),
+    1024: dict(n=8, N=1024, l=2, bg_bit=14, ks_t=8, ks_basebit=2, alpha_lwe=2**-15, alpha_bk=2**-25),
+    2048: dict(n=8, N=2048, l=2, bg_bit=12, ks_t=8, ks_basebit=2, alpha_lwe=2**-15, alpha_bk=2**-25),
+}
+
+
+@pytest.mark.parametrize("N", sorted(THREE_PARTS))
+def test_blind_rotate_extract_three_key_parts(torch, N):
+    """Blind rotation + SampleExtract with the key split into three parts
+    (one or more ciphertexts per wave at N <= 512, two waves per ciphertext at
+    N = 1024, four at N = 2048): a small batch in full, and a batch large
+    enough for the multi-ciphertext block shape, sampled, against the oracle."""
+    p = THREE_PARTS[N]
+    assert tfhe.tfhe_transform_error_bound(p)[0] == 3
+    sk, ek, ok = keys_for(f"three-parts-{N}", torch, params=p, seed=0x3A3A + N)
+    rng = np.random.default_rng(N)
+    tv = rng.integers(0, M32, N, dtype=np.uint64).astype(np.uint32)
+    for B, sample in ((5, None), (1030, np.array([0, 1, 513, 1029]))):
+        x = rng.integers(0, M32, (B, p["n"] + 1), dtype=np.uint64).astype(np.uint32)
+        say(f"three key parts N={N} B={B}")
+        got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x), tfhe.to_device(tv)))
+        idx = np.arange(B) if sample is None else sample
+        assert np.array_equal(got[idx], oracle.bootstrap_no_ks(ok, x[idx], tv))
+
+
 def test_keyswitch_parity_toy(torch):
     p = wl.CONFIGS["toy"]["params"]
     sk, ek, ok = keys_for("toy", torch)
