@@ -225,6 +225,35 @@ def test_determinism_and_batch_independence(torch):
     assert np.array_equal(np.concatenate(parts), r1)
 
 
+def test_concurrent_calls_on_two_streams(torch):
+    """Two calls in flight at once on two streams (default priority), each
+    with its own workspace and output, give the results of the same calls
+    made one after the other."""
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    rng = np.random.default_rng(23)
+    B = 1024
+    ins = []
+    for k in range(2):
+        a, b = rng.integers(0, 2, B), rng.integers(0, 2, B)
+        ins.append((tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 40 + k, tfhe.encode_bits(a), 0)),
+                    tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 40 + k, tfhe.encode_bits(b), B))))
+    say("sequential reference, 2 x 1024 NAND")
+    ref = [tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb)) for ca, cb in ins]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [torch.empty((B, p["n"] + 1), dtype=torch.int32, device="cuda") for _ in range(2)]
+    wss = [tfhe.alloc_workspace(ek, B) for _ in range(2)]
+    torch.cuda.synchronize()
+    say("two streams at once")
+    for k in range(2):
+        with torch.cuda.stream(streams[k]):
+            tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", *ins[k], out=outs[k], workspace=wss[k], stream=streams[k])
+    torch.cuda.synchronize()
+    for k in range(2):
+        assert np.array_equal(tfhe.to_host(outs[k]), ref[k])
+
+
 def test_relu_toy_all_values(torch):
     """All 256 8-bit values through the ReLU unit on the toy parameters,
     streamed in uneven gate windows."""
