@@ -789,6 +789,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
   if (l * bg_bit < 32) offset += 1u << (31 - l * bg_bit);
   const size_t bk_step = static_cast<size_t>(2 * l) * O * NC;
   const uint32_t voff = static_cast<uint32_t>(tc) * 16u;
+  const bool packed_second = l == 2 && bg_bit <= 10;
 
   for (int i = 0; i < n; i++) {
     const uint32_t a_i = ab[i];
@@ -803,6 +804,10 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
 
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
+      // with two digits of at most 10 bits, the second digit of each of the
+      // lane's 4E coefficients is kept from the first digit's pass (three
+      // fields to a register) instead of being recomputed from LDS
+      uint32_t pk[(4 * E + 2) / 3];
       for (int jj = 0; jj < l; jj++) {
         const uint32_t dpos = static_cast<uint32_t>(32 - (jj + 1) * bg_bit), dw = static_cast<uint32_t>(bg_bit);
         const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
@@ -819,26 +824,52 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
         int t_q = t;
         asm volatile("" : "+v"(a_q), "+v"(t_q));
         double2 x[E];
-        // raised issue priority while the digits' LDS reads are issued (as
-        // in the transposes): measured 7 % faster at N = 2048, where the
-        // two waves of a ciphertext wait on each other at the block barriers
-        __builtin_amdgcn_s_setprio(3);
+        if (packed_second && jj == 1) {
+          // the second digits, kept from the first digit's pass
 #pragma unroll
-        for (int e = 0; e < E; e++) {
-          double dg[2][2];
+          for (int e = 0; e < E; e++) {
+            double dg[2][2];
 #pragma unroll
-          for (int hh = 0; hh < 2; hh++)
+            for (int hh = 0; hh < 2; hh++)
 #pragma unroll
-            for (int im = 0; im < 2; im++) {
-              const int j = t_q + 64 * e + hh * HN + im * NC;
-              const uint32_t D = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
-              dg[hh][im] = static_cast<double>(signed_field(D, dpos, dw));
-            }
-          const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
-          x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
-                              fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+              for (int im = 0; im < 2; im++) {
+                const int k = (e * 2 + hh) * 2 + im;
+                dg[hh][im] = static_cast<double>(signed_field(pk[k / 3], 10u * (k % 3), dw));
+              }
+            const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
+            x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
+                                fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+          }
+        } else {
+          // raised issue priority while the digits' LDS reads are issued (as
+          // in the transposes): measured 7 % faster at N = 2048, where the
+          // two waves of a ciphertext wait on each other at the block barriers
+          __builtin_amdgcn_s_setprio(3);
+          const uint32_t dpos2 = dpos - dw;  // the second digit's field
+#pragma unroll
+          for (int e = 0; e < E; e++) {
+            double dg[2][2];
+#pragma unroll
+            for (int hh = 0; hh < 2; hh++)
+#pragma unroll
+              for (int im = 0; im < 2; im++) {
+                const int j = t_q + 64 * e + hh * HN + im * NC;
+                const uint32_t D = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
+                dg[hh][im] = static_cast<double>(signed_field(D, dpos, dw));
+                if (packed_second) {
+                  // the second digit's field (its sign extension is the
+                  // digit, as for the first) packed three to a register
+                  const int k = (e * 2 + hh) * 2 + im;
+                  const uint32_t f = __builtin_amdgcn_ubfe(D, dpos2, dw);
+                  pk[k / 3] = k % 3 ? pk[k / 3] | (f << (10u * (k % 3))) : f;
+                }
+              }
+            const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
+            x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
+                                fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+          }
+          __builtin_amdgcn_s_setprio(0);
         }
-        __builtin_amdgcn_s_setprio(0);
         fft_forward<Sub, true, true>(x, t, scr, tw_half, tw_g, 2 + h);
 #pragma unroll
         for (int o = 0; o < O; o++) {
