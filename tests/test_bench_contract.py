@@ -1,0 +1,49 @@
+"""bench.py's contract, checked on the CPU: one GPU only, and the
+algorithmic operation count of the blind rotation written out by hand."""
+import math
+import os
+import subprocess
+import sys
+
+import bench
+from paper_1911_07101_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr
+
+
+def _lane_ops_by_stage(N, n_lwe, l, parts):
+    """Per CMux, stage by stage, for the 128-bit parameters' shape: 2l forward
+    transforms, the transform-domain products, 2 x parts inverse transforms
+    with their twist, digit extraction, the rotation difference and the
+    rounding (one VALU lane-operation per FMA, add or integer op)."""
+    n = N // 2                      # complex points of the folded polynomial
+    stages = int(math.log2(n))
+    butterflies = n // 2 * stages
+    forward = 2 * l * butterflies * 6
+    products = 2 * l * (2 * parts) * n * 4
+    # inverse: stage s has n/2 butterflies, of which those with twiddle 1 or
+    # -i (n/2 at stage 0, n/2^(s+1) ... counted as n >> s for s >= 1) take 4
+    inverse_one = 0
+    for s in range(stages):
+        trivial = n // 2 if s == 0 else n >> s
+        inverse_one += (n // 2 - trivial) * 6 + trivial * 4
+    inverse = 2 * parts * (inverse_one + 4 * n)
+    digits = 2 * l * N * 4
+    rotation = 2 * N * 3
+    rounding = 2 * N * 2 * parts
+    return n_lwe * (forward + products + inverse + digits + rotation + rounding)
+
+
+def test_algorithmic_count_matches_a_stage_by_stage_count():
+    for name in ("tfhe128_nand", "lut3_n2048", "toy"):
+        p = wl.CONFIGS[name]["params"]
+        assert bench.algorithmic_lane_ops(p, 2) == _lane_ops_by_stage(p["N"], p["n"], p["l"], 2)
+    # the figure the roofline is quoted on
+    assert bench.algorithmic_lane_ops(wl.CONFIGS["tfhe128_nand"]["params"], 2) == 143_871_840
