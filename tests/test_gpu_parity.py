@@ -159,6 +159,34 @@ def test_blind_rotate_extract_three_key_parts(torch, N):
         assert np.array_equal(got[idx], oracle.bootstrap_no_ks(ok, x[idx], tv))
 
 
+def test_parameter_and_batch_limits(torch):
+    """The largest LWE dimension the library accepts (n = 4096, here with the
+    toy ring) and a batch of 100,003 gates (many rounds of blocks and a
+    ragged last block), sampled against the oracle; every output decrypts to
+    its truth table."""
+    p = dict(n=4096, N=256, l=3, bg_bit=7, ks_t=8, ks_basebit=2, alpha_lwe=2**-15, alpha_bk=2**-25)
+    sk, ek, ok = keys_for("n-4096", torch, params=p, seed=0x4096)
+    a, b = np.array([0, 1, 1, 0, 1]), np.array([1, 1, 0, 0, 1])
+    ca = tfhe.tfhe_encrypt_torus(sk, 5, tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, 5, tfhe.encode_bits(b), len(a))
+    say("n = 4096, 5 NAND")
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", tfhe.to_device(ca), tfhe.to_device(cb)))
+    assert np.array_equal(got, oracle.gate_bootstrap(ok, "NAND", ca, cb))
+    assert np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, got)), 1 - (a & b))
+
+    cfg = wl.CONFIGS["toy"]
+    sk, ek, ok = keys_for("toy", torch)
+    B = 100_003
+    a, b = wl.gate_inputs(cfg["input_seed"] + 9, B)
+    ca = tfhe.tfhe_encrypt_torus(sk, 9, tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, 9, tfhe.encode_bits(b), B)
+    say(f"toy, {B} NOR")
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NOR", tfhe.to_device(ca), tfhe.to_device(cb)))
+    assert np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, got)), 1 - (a | b))
+    idx = np.array([0, 1, 4095, 4096, 65535, 65536, B - 2, B - 1])
+    assert np.array_equal(got[idx], oracle.gate_bootstrap(ok, "NOR", ca[idx], cb[idx]))
+
+
 def test_keyswitch_parity_toy(torch):
     p = wl.CONFIGS["toy"]["params"]
     sk, ek, ok = keys_for("toy", torch)
