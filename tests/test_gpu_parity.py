@@ -303,6 +303,24 @@ def test_relu_toy_all_values(torch):
     assert np.array_equal(wl.from_bits(dec), np.maximum(xs, 0))
 
 
+@pytest.mark.parametrize("bits", [2, 5, 16])
+def test_relu_toy_other_widths(torch, bits):
+    """The ReLU unit on values of other bit widths (the unit has bits - 1
+    gates per value and a trivial sign), against the oracle and max(x, 0)."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    rng = np.random.default_rng(200 + bits)
+    lo, hi = -(1 << (bits - 1)), 1 << (bits - 1)
+    xs = np.concatenate([[lo, -1, 0, hi - 1], rng.integers(lo, hi, 29)])
+    ct = tfhe.tfhe_encrypt_torus(sk, 60 + bits, tfhe.encode_bits(wl.to_bits(xs, bits).ravel()))
+    ct = ct.reshape(len(xs), bits, p["n"] + 1)
+    say(f"relu toy {len(xs)} values of {bits} bits")
+    got = tfhe.to_host(tfhe.glyph_relu_batch(ek, tfhe.to_device(ct), bits))
+    assert np.array_equal(got, oracle.relu(ok, ct, bits))
+    dec = bits_of(tfhe.tfhe_decrypt_phase(sk, got.reshape(-1, p["n"] + 1))).reshape(len(xs), bits)
+    assert np.array_equal(wl.from_bits(dec), np.maximum(xs, 0))
+
+
 def test_irelu_toy_all_4bit_pairs(torch):
     """Backward iReLU for every (4-bit u, 4-bit delta) pair on the toy
     parameters, in uneven gate windows: bit-exact with the oracle, and every
@@ -430,6 +448,49 @@ def test_bootstrap_onto_multiples_of_inverse_modulus_n2048(torch):
 
 
 # ---------------------------------------------------- full-size workloads
+
+@pytest.mark.parametrize("msg_bits", [1, 2, 3])
+def test_lut_bootstrap_n1024(torch, msg_bits):
+    """Table-lookup bootstraps (+ key switching) at the 128-bit parameters
+    (N = 1024) with 1-, 2- and 3-bit tables: bit for bit against the oracle,
+    and every output decrypts to its table entry (a 3-bit output's half box,
+    1/32, is ~6.7 output standard deviations at these parameters)."""
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    rng = np.random.default_rng(300 + msg_bits)
+    M = 1 << msg_bits
+    table = rng.integers(0, M, M).astype(np.uint32)
+    m = np.resize(np.arange(M), 67).astype(np.uint32)
+    tv = tfhe.tfhe_lut_testvec(p["N"], msg_bits, table)
+    assert np.array_equal(tv, oracle.lut_testvec(p["N"], msg_bits, table))
+    shift = 31 - msg_bits
+    ct = tfhe.tfhe_encrypt_torus(sk, 70 + msg_bits, (m << shift).astype(np.uint32))
+    say(f"lut bootstrap N=1024 msg_bits={msg_bits} B={len(m)}")
+    got = tfhe.to_host(tfhe.tfhe_lut_bootstrap_batch(ek, tfhe.to_device(ct), tfhe.to_device(tv)))
+    ph = tfhe.tfhe_decrypt_phase(sk, got).astype(np.int64)
+    assert np.array_equal(((ph + (1 << (shift - 1))) >> shift) & (2 * M - 1), table[m])
+    idx = np.array([0, 1, M - 1, len(m) - 1])
+    assert np.array_equal(got[idx], oracle.lut_bootstrap(ok, ct[idx], tv))
+
+
+@pytest.mark.parametrize("gate", list(TRUTH))
+def test_gate_bootstrap_128bit(torch, gate):
+    """Every gate at the 128-bit parameters: all outputs decrypt to the truth
+    table, a sample matches the oracle bit for bit."""
+    p = wl.CONFIGS["tfhe128_nand"]["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    rng = np.random.default_rng(400 + list(TRUTH).index(gate))
+    B = 96
+    a, b = rng.integers(0, 2, B), rng.integers(0, 2, B)
+    ca = tfhe.tfhe_encrypt_torus(sk, 80, tfhe.encode_bits(a), 0)
+    cb = tfhe.tfhe_encrypt_torus(sk, 80, tfhe.encode_bits(b), B)
+    say(f"{gate} 128-bit B={B}")
+    got = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, gate, tfhe.to_device(ca), tfhe.to_device(cb)))
+    assert np.array_equal(bits_of(tfhe.tfhe_decrypt_phase(sk, got)), TRUTH[gate](a, b))
+    idx = np.array([0, 37, B - 1])
+    assert np.array_equal(got[idx], oracle.gate_bootstrap(ok, gate, ca[idx], cb[idx]))
+
 
 def test_tfhe128_nand_4096(torch):
     cfg = wl.CONFIGS["tfhe128_nand"]
