@@ -1089,55 +1089,67 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
 }
 
 // Key switching for t = 8 digits of 2 bits (16-bit precision), one sample per
-// thread.  A block of 256 threads covers 256 samples and KS8_COLS output
+// thread.  A block of 256 threads covers 256 samples and COLS output
 // columns.  For each input coefficient i the block builds, in LDS, the pair
 // tables
 //   PT[p][u][col] = KSK[i][2p][u >> 2] + KSK[i][2p+1][u & 3]   (row of value 0 = 0)
 // for the 4 digit pairs p and the 16 pair values u; a thread then reads, for
 // each of its 4 pair values, the table row of that value with 16-byte loads
-// (4 columns each) and subtracts the 4 rows from its KS8_COLS outputs.  The
+// (4 columns each) and subtracts the 4 rows from its COLS outputs.  The
 // digits are taken once per sample and input coefficient, the row addresses
 // once per pair, and the column offsets are immediates.  Tables are
 // double-buffered across i (one barrier per i); the key rows are fetched
 // ahead.  Every table read, add and the final subtraction are exact
 // mod 2^32.
-constexpr int KS8_COLS = 16;               // output columns per block
-constexpr int KS8_RS = KS8_COLS + 4;       // padded table row stride (words)
 constexpr int KS8_TAB = 64;                // 4 pairs x 16 pair values
 
+template <int COLS>
 __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __restrict__ in,
                                                              const uint32_t* __restrict__ ksk,
                                                              uint32_t* __restrict__ out, int n, int N,
                                                              int64_t B, int mode, int32_t bits,
                                                              int64_t gate_begin) {
   constexpr int ROWS = 24;  // 8 digits x 3 non-zero values
-  __shared__ __align__(16) uint32_t s_tab[2][KS8_TAB * KS8_RS];
+  constexpr int RS = COLS + 4;   // padded table row stride (words)
+  constexpr int VPT = COLS >= 16 ? 4 : COLS / 4;  // table entries each thread builds per (pair, half)
+  constexpr int PPT = COLS >= 16 ? COLS / 16 : 1;  // pairs each thread builds for
+  __shared__ __align__(16) uint32_t s_tab[2][KS8_TAB * RS];
   const int tid = threadIdx.x;
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + tid;
   const bool c_ok = c < B;
-  const int col0 = blockIdx.y * KS8_COLS;
+  const int col0 = blockIdx.y * COLS;
   const size_t row = static_cast<size_t>(n) + 1;
   const uint32_t* x_in = in + (c_ok ? c : B - 1) * (N + 1);
 
-  uint32_t acc[KS8_COLS];
+  uint32_t acc[COLS];
 #pragma unroll
-  for (int j = 0; j < KS8_COLS; j++) acc[j] = col0 + j == n ? x_in[N] : 0u;
+  for (int j = 0; j < COLS; j++) acc[j] = col0 + j == n ? x_in[N] : 0u;
 
-  // table building: thread (p, col, half) = (tid >> 6 & 3, tid & 15, tid >> 4 & 3)
-  // fetches key rows of pair p at column col0 + col and writes the 4 entries
-  // u = 4 * half + v2: PT[p][u] = row(2p, half) + row(2p+1, v2), row(., 0) = 0
-  const int b_col = tid & 15, b_half = (tid >> 4) & 3, b_pair = tid >> 6;
+  // table building: thread (p, col, half, g) = (tid / 4COLS % 4, tid % COLS,
+  // tid / COLS % 4, tid / 16COLS) fetches key rows of pair p at column
+  // col0 + col and writes the VPT entries u = 4 * half + v2, v2 in
+  // [g VPT, g VPT + VPT): PT[p][u] = row(2p, half) + row(2p+1, v2), row(., 0) = 0
+  const int b_col = tid % COLS, b_half = (tid / COLS) % 4, b_pair = (tid / (4 * COLS)) % 4;
+  const int b_v2 = COLS >= 16 ? 0 : (tid / (16 * COLS)) * VPT;
   const bool b_ok = col0 + b_col <= n;
   // key rows of coefficient i + d in kr[d] (element 0: row(2p, half),
-  // elements 1..3: row(2p+1, 1..3)) and inputs x_i+d in xq[d]: both are
+  // element 1 + v: row(2p+1, b_v2 + v)) and inputs x_i+d in xq[d]: both are
   // fetched ahead (key rows three coefficients, inputs four), so their
   // latency is covered by the table lookups in between
-  uint32_t kr[3][4];
-  auto fetch = [&](int i, uint32_t (&k)[4]) {
+  uint32_t kr[3][PPT][VPT + 1];
+  auto fetch = [&](int i, uint32_t (&kk)[PPT][VPT + 1]) {
     const uint32_t* base = ksk + static_cast<size_t>(i) * ROWS * row + col0 + b_col;
-    k[0] = (b_ok && b_half) ? base[static_cast<size_t>(b_pair * 6 + b_half - 1) * row] : 0u;
 #pragma unroll
-    for (int v = 1; v <= 3; v++) k[v] = b_ok ? base[static_cast<size_t>(b_pair * 6 + 2 + v) * row] : 0u;
+    for (int pp = 0; pp < PPT; pp++) {
+      const int pr = b_pair + pp * (4 / PPT);
+      uint32_t (&k)[VPT + 1] = kk[pp];
+      k[0] = (b_ok && b_half) ? base[static_cast<size_t>(pr * 6 + b_half - 1) * row] : 0u;
+#pragma unroll
+      for (int v = 0; v < VPT; v++) {
+        const int v2 = b_v2 + v;
+        k[1 + v] = (b_ok && v2) ? base[static_cast<size_t>(pr * 6 + 2 + v2) * row] : 0u;
+      }
+    }
   };
   for (int d = 0; d < 3; d++) fetch(min(d, N - 1), kr[d]);
   uint32_t xq[4];
@@ -1147,16 +1159,19 @@ __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __r
 #pragma unroll 1
   for (int i = 0; i < N; i++) {
     const int b = i & 1;
-    {
-      uint32_t* tab = s_tab[b] + (b_pair * 16 + b_half * 4) * KS8_RS + b_col;
 #pragma unroll
-      for (int v2 = 0; v2 < 4; v2++) tab[v2 * KS8_RS] = kr[0][0] + (v2 ? kr[0][v2] : 0u);
+    for (int pp = 0; pp < PPT; pp++) {
+      uint32_t* tab = s_tab[b] + ((b_pair + pp * (4 / PPT)) * 16 + b_half * 4 + b_v2) * RS + b_col;
+#pragma unroll
+      for (int v = 0; v < VPT; v++) tab[v * RS] = kr[0][pp][0] + kr[0][pp][1 + v];
     }
     const uint32_t x = xq[0];
 #pragma unroll
     for (int d = 0; d < 2; d++)
 #pragma unroll
-      for (int v = 0; v < 4; v++) kr[d][v] = kr[d + 1][v];
+      for (int pp = 0; pp < PPT; pp++)
+#pragma unroll
+        for (int v = 0; v <= VPT; v++) kr[d][pp][v] = kr[d + 1][pp][v];
     fetch(min(i + 3, N - 1), kr[2]);
 #pragma unroll
     for (int d = 0; d < 3; d++) xq[d] = xq[d + 1];
@@ -1167,9 +1182,9 @@ __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __r
     const uint4* rp[4];
 #pragma unroll
     for (int p = 0; p < 4; p++)
-      rp[p] = reinterpret_cast<const uint4*>(tab + (p * 16 + ((r >> (12 - 4 * p)) & 15)) * KS8_RS);
+      rp[p] = reinterpret_cast<const uint4*>(tab + (p * 16 + ((r >> (12 - 4 * p)) & 15)) * RS);
 #pragma unroll
-    for (int q = 0; q < KS8_COLS / 4; q++) {
+    for (int q = 0; q < COLS / 4; q++) {
       const uint4 s0 = rp[0][q], s1 = rp[1][q], s2 = rp[2][q], s3 = rp[3][q];
       acc[4 * q + 0] -= (s0.x + s1.x) + (s2.x + s3.x);
       acc[4 * q + 1] -= (s0.y + s1.y) + (s2.y + s3.y);
@@ -1181,7 +1196,7 @@ __global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __r
   if (!c_ok) return;
   uint32_t* o = out + out_index(mode, c, bits, gate_begin) * row + col0;
 #pragma unroll
-  for (int j = 0; j < KS8_COLS; j++)
+  for (int j = 0; j < COLS; j++)
     if (col0 + j <= n) o[j] = acc[j];
 }
 
@@ -1479,9 +1494,21 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
   dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (p.ks_t == 8 && p.ks_basebit == 2) {
-    dim3 g8(static_cast<unsigned>((B + 255) / 256), static_cast<unsigned>((p.n + 1 + KS8_COLS - 1) / KS8_COLS));
-    hipLaunchKernelGGL(keyswitch_t8b2_kernel, g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
-                       bits, gate_begin);
+    // 32 output columns per block halve the table building and barriers per
+    // output, but only pay while the grid still gives every CU two blocks
+    // (4096 samples at n = 630: 16 columns, 0.87 ms against 1.02; 8192 at
+    // n = 750: 32 columns, 2.57 ms against 4.15)
+    const int64_t cus = ek->cus > 0 ? ek->cus : 256;
+    const int64_t sample_blocks = (B + 255) / 256;
+    if (sample_blocks * ((p.n + 1 + 31) / 32) >= 2 * cus) {
+      dim3 g8(static_cast<unsigned>(sample_blocks), static_cast<unsigned>((p.n + 1 + 31) / 32));
+      hipLaunchKernelGGL((keyswitch_t8b2_kernel<32>), g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
+                         bits, gate_begin);
+    } else {
+      dim3 g8(static_cast<unsigned>(sample_blocks), static_cast<unsigned>((p.n + 1 + 15) / 16));
+      hipLaunchKernelGGL((keyswitch_t8b2_kernel<16>), g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
+                         bits, gate_begin);
+    }
   } else if (p.ks_t * (1 << p.ks_basebit) <= 32)
     hipLaunchKernelGGL((keyswitch_kernel<32>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
                        p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);
