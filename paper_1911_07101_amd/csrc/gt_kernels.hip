@@ -483,8 +483,11 @@ struct BrCfg {
   static constexpr bool ITW_LDS = CPB > 1 && T <= 64;
   static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4 + (ITW_LDS ? (NC - 1) * 16 : 0);
   static_assert(LDS_BYTES <= 160 * 1024, "block exceeds the CU's LDS");
-  // compiled for two waves per SIMD (256 VGPRs per wave)
-  static constexpr int MIN_WAVES = 2;
+  // compiled for two waves per SIMD (256 VGPRs per wave); blocks of at most
+  // 4 waves are launched only when each SIMD gets at most one wave, and
+  // compiled for one (the compiler may then also use accumulation registers:
+  // 256 gates 8.94 -> 8.31 ms)
+  static constexpr int MIN_WAVES = WPB <= 4 ? 1 : 2;
 };
 
 // 16-byte load through a buffer resource (base and size uniform, offset per
