@@ -124,6 +124,26 @@ def _dptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _dbuf(t, words: int, name: str, device=None):
+    """Device pointer of a buffer of at least `words` 32-bit words: the C ABI
+    takes plain pointers, so sizes, element width and device are checked
+    here, before any kernel can touch memory outside the tensor."""
+    if t.element_size() != 4:
+        raise ValueError(f"{name}: expected 32-bit elements, got {t.dtype}")
+    if t.numel() < words:
+        raise ValueError(f"{name}: {t.numel()} words, the call needs {words}")
+    if device is not None and t.is_cuda and t.device.index != device:
+        raise ValueError(f"{name}: on cuda:{t.device.index}, the key is on cuda:{device}")
+    return _dptr(t)
+
+
+def _wsbuf(ws, device):
+    """(pointer, size in bytes) of a workspace tensor on the key's device."""
+    if ws.is_cuda and ws.device.index != device:
+        raise ValueError(f"workspace: on cuda:{ws.device.index}, the key is on cuda:{device}")
+    return _dptr(ws), ws.numel() * ws.element_size()
+
+
 def _stream(stream):
     import torch
     if stream is None:
@@ -274,8 +294,10 @@ def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=Non
     out = _empty((B, n + 1), ek) if out is None else out
     ws = alloc_workspace(ek, B) if workspace is None else workspace
     g = GATES[gate] if isinstance(gate, str) else int(gate)
-    _check(lib().tfhe_gate_bootstrap_batch(ek.handle, g, _dptr(ca), _dptr(cb), _dptr(out), B,
-                                           _dptr(ws), ws.numel(), _stream(stream)))
+    w = B * (n + 1)
+    d = ek.device
+    _check(lib().tfhe_gate_bootstrap_batch(ek.handle, g, _dbuf(ca, w, "ca", d), _dbuf(cb, w, "cb", d),
+                                           _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
     return out
 
 
@@ -283,8 +305,9 @@ def tfhe_lut_bootstrap_batch(ek: EvalKey, x, testvec, out=None, workspace=None, 
     B = x.shape[0]
     out = _empty((B, ek.params.n + 1), ek) if out is None else out
     ws = alloc_workspace(ek, B) if workspace is None else workspace
-    _check(lib().tfhe_lut_bootstrap_batch(ek.handle, _dptr(x), _dptr(testvec), _dptr(out), B,
-                                          _dptr(ws), ws.numel(), _stream(stream)))
+    w, d = B * (ek.params.n + 1), ek.device
+    _check(lib().tfhe_lut_bootstrap_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(testvec, ek.params.N, "testvec", d),
+                                          _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
     return out
 
 
@@ -292,16 +315,20 @@ def tfhe_bootstrap_extract_batch(ek: EvalKey, x, testvec=None, out=None, workspa
     B = x.shape[0]
     out = _empty((B, ek.params.N + 1), ek) if out is None else out
     ws = alloc_workspace(ek, B) if workspace is None else workspace
-    tv = _dptr(testvec) if testvec is not None else ctypes.c_void_p(0)
-    _check(lib().tfhe_bootstrap_extract_batch(ek.handle, _dptr(x), tv, _dptr(out), B, _dptr(ws),
-                                              ws.numel(), _stream(stream)))
+    p, d = ek.params, ek.device
+    tv = _dbuf(testvec, p.N, "testvec", d) if testvec is not None else ctypes.c_void_p(0)
+    _check(lib().tfhe_bootstrap_extract_batch(ek.handle, _dbuf(x, B * (p.n + 1), "x", d), tv,
+                                              _dbuf(out, B * (p.N + 1), "out", d), B, *_wsbuf(ws, d),
+                                              _stream(stream)))
     return out
 
 
 def tfhe_keyswitch_batch(ek: EvalKey, x, out=None, stream=None):
     B = x.shape[0]
     out = _empty((B, ek.params.n + 1), ek) if out is None else out
-    _check(lib().tfhe_keyswitch_batch(ek.handle, _dptr(x), _dptr(out), B, _stream(stream)))
+    p, d = ek.params, ek.device
+    _check(lib().tfhe_keyswitch_batch(ek.handle, _dbuf(x, B * (p.N + 1), "x", d),
+                                      _dbuf(out, B * (p.n + 1), "out", d), B, _stream(stream)))
     return out
 
 
@@ -313,8 +340,9 @@ def glyph_relu_batch(ek: EvalKey, x, bits: int, y=None, gate_begin: int = 0, gat
     if gate_end is None:
         gate_end = V * (bits - 1)
     ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
-    _check(lib().glyph_relu_batch(ek.handle, _dptr(x), _dptr(y), V, bits, gate_begin, gate_end,
-                                  _dptr(ws), ws.numel(), _stream(stream)))
+    w, d = V * bits * (n + 1), ek.device
+    _check(lib().glyph_relu_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(y, w, "y", d), V, bits, gate_begin,
+                                  gate_end, *_wsbuf(ws, d), _stream(stream)))
     return y
 
 
@@ -328,8 +356,10 @@ def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate
     if gate_end is None:
         gate_end = V * bits
     ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
-    _check(lib().glyph_irelu_batch(ek.handle, _dptr(u), u_bits, _dptr(delta), _dptr(out), V, bits,
-                                   gate_begin, gate_end, _dptr(ws), ws.numel(), _stream(stream)))
+    row, d = ek.params.n + 1, ek.device
+    _check(lib().glyph_irelu_batch(ek.handle, _dbuf(u, V * u_bits * row, "u", d), u_bits,
+                                   _dbuf(delta, V * bits * row, "delta", d), _dbuf(out, V * bits * row, "out", d),
+                                   V, bits, gate_begin, gate_end, *_wsbuf(ws, d), _stream(stream)))
     return out
 
 
@@ -338,8 +368,9 @@ def tfhe_mux_batch(ek: EvalKey, c, a, b, out=None, workspace=None, stream=None):
     B = c.shape[0]
     out = _empty((B, ek.params.n + 1), ek) if out is None else out
     ws = alloc_workspace(ek, 2 * B) if workspace is None else workspace
-    _check(lib().tfhe_mux_batch(ek.handle, _dptr(c), _dptr(a), _dptr(b), _dptr(out), B, _dptr(ws),
-                                ws.numel(), _stream(stream)))
+    w, d = B * (ek.params.n + 1), ek.device
+    _check(lib().tfhe_mux_batch(ek.handle, _dbuf(c, w, "c", d), _dbuf(a, w, "a", d), _dbuf(b, w, "b", d),
+                                _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
     return out
 
 
@@ -366,8 +397,10 @@ def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspac
         raise ValueError(f"table needs {1 << msg_bits} entries")
     out = _empty((V, out_bits, ek.params.n + 1), ek) if out is None else out
     ws = alloc_mux_lut_workspace(ek, V, msg_bits, out_bits) if workspace is None else workspace
-    _check(lib().glyph_mux_lut_batch(ek.handle, _dptr(x), msg_bits, _hptr(t), out_bits, _dptr(out), V,
-                                     _dptr(ws), ws.numel(), _stream(stream)))
+    row, d = ek.params.n + 1, ek.device
+    _check(lib().glyph_mux_lut_batch(ek.handle, _dbuf(x, V * msg_bits * row, "x", d), msg_bits, _hptr(t), out_bits,
+                                     _dbuf(out, V * out_bits * row, "out", d), V, *_wsbuf(ws, d),
+                                     _stream(stream)))
     return out
 
 
@@ -386,7 +419,9 @@ def tfhe_pack_keyswitch_batch(ek: EvalKey, lwe, out=None, stream=None):
     """lwe [B][Z][n+1] -> TRLWE samples [B][2][N] (phase sum_z phase_z X^z)."""
     B, Z = lwe.shape[0], lwe.shape[1]
     out = _empty((B, 2, ek.params.N), ek) if out is None else out
-    _check(lib().tfhe_pack_keyswitch_batch(ek.handle, _dptr(lwe), Z, _dptr(out), B, _stream(stream)))
+    p, d = ek.params, ek.device
+    _check(lib().tfhe_pack_keyswitch_batch(ek.handle, _dbuf(lwe, B * Z * (p.n + 1), "lwe", d), Z,
+                                           _dbuf(out, B * 2 * p.N, "out", d), B, _stream(stream)))
     return out
 
 
@@ -395,7 +430,9 @@ def tfhe_sample_extract_batch(trlwe, K: int, out=None, stream=None):
     import torch
     B, N = trlwe.shape[0], trlwe.shape[2]
     out = torch.empty((B, K, N + 1), dtype=torch.int32, device=trlwe.device) if out is None else out
-    _check(lib().tfhe_sample_extract_batch(N, _dptr(trlwe), B, K, _dptr(out), _stream(stream)))
+    d = trlwe.device.index
+    _check(lib().tfhe_sample_extract_batch(N, _dbuf(trlwe, B * 2 * N, "trlwe", d), B, K,
+                                           _dbuf(out, B * K * (N + 1), "out", d), _stream(stream)))
     return out
 
 
@@ -411,7 +448,9 @@ def tfhe_not_batch(x, out=None, stream=None):
     dim = x.shape[-1] - 1
     count = x.numel() // (dim + 1)
     out = torch.empty_like(x) if out is None else out
-    _check(lib().tfhe_not_batch(dim, _dptr(x), _dptr(out), count, _stream(stream)))
+    w = count * (dim + 1)
+    _check(lib().tfhe_not_batch(dim, _dbuf(x, w, "x"), _dbuf(out, w, "out", x.device.index), count,
+                                _stream(stream)))
     return out
 
 
@@ -419,8 +458,9 @@ def tfhe_negacyclic_mul_batch(ek: EvalKey, d, b, out=None, stream=None):
     import torch
     B = d.shape[0]
     out = torch.empty_like(b) if out is None else out
-    _check(lib().tfhe_negacyclic_mul_batch(ek.handle, _dptr(d), _dptr(b), _dptr(out), B,
-                                           _stream(stream)))
+    w, dev = B * ek.params.N, ek.device
+    _check(lib().tfhe_negacyclic_mul_batch(ek.handle, _dbuf(d, w, "d", dev), _dbuf(b, w, "b", dev),
+                                           _dbuf(out, w, "out", dev), B, _stream(stream)))
     return out
 
 

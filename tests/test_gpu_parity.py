@@ -764,6 +764,10 @@ def test_empty_and_invalid_calls(torch):
     with pytest.raises(tfhe.TfheError) as ei:  # entry 9 does not fit in 3 output bits
         tfhe.glyph_mux_lut_batch(ek, x3, np.array([0, 1, 2, 3, 4, 5, 6, 9]), 3)
     assert ei.value.rc == tfhe.TFHE_EINVAL
+    with pytest.raises(ValueError):  # rows of n = 64 words where the key needs n + 1
+        tfhe.tfhe_gate_bootstrap_batch(ek, "AND", x[:, :row - 1].contiguous(), x[:, :row - 1].contiguous())
+    with pytest.raises(ValueError):  # 64-bit elements
+        tfhe.tfhe_keyswitch_batch(ek, torch.zeros((4, p["N"] + 1), dtype=torch.int64, device="cuda:0"))
     sk2, ek2 = tfhe.tfhe_keygen_from_seed(p, 5, 0)  # fresh key without a packing key
     with pytest.raises(tfhe.TfheError) as ei:
         tfhe.tfhe_pack_keyswitch_batch(ek2, tfhe.to_device(np.zeros((1, 3, row), np.uint32)))

@@ -137,3 +137,15 @@ def test_torus_testvec_matches_oracle():
     for N, bits in [(256, 3), (1024, 3), (2048, 5)]:
         vals = rng.integers(0, 1 << 32, 1 << bits, dtype=np.uint64).astype(np.uint32)
         assert np.array_equal(tfhe.tfhe_torus_testvec(N, bits, vals), oracle.torus_testvec(N, bits, vals))
+
+
+def test_binding_checks_buffers_before_any_call():
+    """The C ABI takes plain pointers, so the binding checks element width,
+    size and placement of every device buffer before calling it."""
+    import torch
+    with pytest.raises(ValueError, match="32-bit"):
+        tfhe._dbuf(torch.zeros(8, dtype=torch.int64), 8, "x")
+    with pytest.raises(ValueError, match="needs 8"):
+        tfhe._dbuf(torch.zeros(7, dtype=torch.int32), 8, "x")
+    with pytest.raises(ValueError, match="device tensor"):
+        tfhe._dbuf(torch.zeros(8, dtype=torch.int32), 8, "x")
