@@ -67,10 +67,16 @@ def kernel_source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(digest: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "blind_rotate_tfhe128_traffic.json")
+TRAFFIC_FILES = {"tfhe128_nand": "blind_rotate_tfhe128_traffic.json",
+                 "lut3_n2048": "blind_rotate_split_lut3_n2048_traffic.json"}
+
+
+def measured_traffic(digest: str, config: str = "tfhe128_nand"):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of
+    the workload, if it was taken on the current kernel source."""
+    if config not in TRAFFIC_FILES:
+        return None
+    path = os.path.join(ROOT, "profiles", TRAFFIC_FILES[config])
     if not os.path.exists(path):
         return None
     with open(path) as fh:
@@ -92,7 +98,10 @@ def host_cpu_model() -> str:
     return platform.processor() or platform.machine()
 
 
-def cpu_baseline(cfg, ca, cb, gpu_out):
+def cpu_baseline(cfg, ca, cb, gpu_out, testvec=None):
+    """The oracle on the first gates (or lookups) of the batch.  ca, cb: the
+    gate inputs; for a table-lookup workload ca holds the inputs and testvec
+    the test polynomial."""
     import numpy as np
 
     import oracle
@@ -100,15 +109,22 @@ def cpu_baseline(cfg, ca, cb, gpu_out):
 
     p = cfg["params"]
     threads = oracle.threads()
-    count = int(min(128, max(8, 6 * threads)))  # about 15 s of oracle work on 16 cores
     keys = oracle.Keys(p, cfg["key_seed"])
-    t0 = time.perf_counter()
-    ref = oracle.gate_bootstrap(keys, cfg["gate"], ca[:count], cb[:count])
+    if testvec is None:
+        count = int(min(128, max(8, 6 * threads)))  # about 15 s of oracle work on 16 cores
+        what = f"{cfg['gate']} gates"
+        t0 = time.perf_counter()
+        ref = oracle.gate_bootstrap(keys, cfg["gate"], ca[:count], cb[:count])
+    else:
+        count = int(min(64, max(4, 2 * threads)))  # N = 2048: ~3x the work per bootstrap
+        what = "table lookups"
+        t0 = time.perf_counter()
+        ref = oracle.lut_bootstrap(keys, ca[:count], testvec)
     dt = time.perf_counter() - t0
     return {
         "value": count / dt, "unit": "bootstraps/s", "cores": threads, "kind": "oracle",
-        "sample": f"first {count} {cfg['gate']} gates of the batch (schoolbook products, "
-                  f"OpenMP over gates), {dt:.1f} s wall",
+        "sample": f"first {count} {what} of the batch (schoolbook products, "
+                  f"OpenMP over bootstraps), {dt:.1f} s wall",
         "host_cpu": host_cpu_model(),
         "core_seconds_per_bootstrap": dt * threads / count,
         "matches_gpu": bool(np.array_equal(ref, tfhe.to_host(gpu_out)[:count])),
@@ -362,20 +378,34 @@ def main():
     from paper_1911_07101_amd import tfhe, workloads as wl
 
     cfg = dict(wl.CONFIGS[args.config])
-    if cfg["kind"] != "gate":
-        raise SystemExit("bench.py times gate-bootstrap workloads")
+    if cfg["kind"] not in ("gate", "lut"):
+        raise SystemExit("bench.py times gate-bootstrap and table-lookup workloads")
     p = cfg["params"]
     B = args.batch or cfg["batch"]
     dev = torch.device("cuda:0")
 
     sk, ek = tfhe.tfhe_keygen_from_seed(p, cfg["key_seed"], 0)
-    a, b = wl.gate_inputs(cfg["input_seed"], B)
-    ca_h = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
-    cb_h = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), B)
-    ca, cb = tfhe.to_device(ca_h), tfhe.to_device(cb_h)
     out = torch.empty((B, p["n"] + 1), dtype=torch.int32, device=dev)
     ws = tfhe.alloc_workspace(ek, B)
     stream = torch.cuda.current_stream()
+    tv_h = None
+    if cfg["kind"] == "gate":
+        a, b = wl.gate_inputs(cfg["input_seed"], B)
+        ca_h = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(a), 0)
+        cb_h = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], tfhe.encode_bits(b), B)
+        ca, cb = tfhe.to_device(ca_h), tfhe.to_device(cb_h)
+        step = lambda: tfhe.tfhe_gate_bootstrap_batch(ek, cfg["gate"], ca, cb, out=out, workspace=ws, stream=stream)
+    else:
+        # 3-bit messages m (encoded m / 16, one padding bit) looked up in a
+        # seeded random 8-entry table by one programmable bootstrap each
+        m = wl.messages(cfg["input_seed"], B, cfg["msg_bits"])
+        table = wl.lut(cfg["input_seed"], cfg["msg_bits"])
+        tv_h = tfhe.tfhe_lut_testvec(p["N"], cfg["msg_bits"], table)
+        tv = tfhe.to_device(tv_h)
+        shift = 31 - cfg["msg_bits"]
+        ca_h, cb_h = tfhe.tfhe_encrypt_torus(sk, cfg["input_seed"], (m << shift).astype(np.uint32), 0), None
+        ca = tfhe.to_device(ca_h)
+        step = lambda: tfhe.tfhe_lut_bootstrap_batch(ek, ca, tv, out=out, workspace=ws, stream=stream)
 
     if args.copy_probe_mib:
         src = torch.empty(args.copy_probe_mib << 18, dtype=torch.int32, device=dev).fill_(1)
@@ -386,7 +416,7 @@ def main():
         del src, dst
 
     for _ in range(args.warmup):
-        tfhe.tfhe_gate_bootstrap_batch(ek, cfg["gate"], ca, cb, out=out, workspace=ws, stream=stream)
+        step()
     torch.cuda.synchronize()
 
     tfhe.tfhe_stage_timing(True)
@@ -396,7 +426,7 @@ def main():
     t0 = time.perf_counter()
     ev[0].record(stream)
     for k in range(args.steps):
-        tfhe.tfhe_gate_bootstrap_batch(ek, cfg["gate"], ca, cb, out=out, workspace=ws, stream=stream)
+        step()
         ev[k + 1].record(stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
@@ -407,9 +437,12 @@ def main():
     elapsed = t1 - t0
     value = B * args.steps / elapsed
     res = tfhe.to_host(out)
-    dec = tfhe.tfhe_decrypt_phase(sk, res).astype(np.int64)
-    dec = (np.where(dec >= 1 << 31, dec - (1 << 32), dec) > 0).astype(np.uint8)
-    truth_ok = bool(np.array_equal(dec, 1 - (a & b))) if cfg["gate"] == "NAND" else None
+    ph = tfhe.tfhe_decrypt_phase(sk, res).astype(np.int64)
+    if cfg["kind"] == "gate":
+        dec = (np.where(ph >= 1 << 31, ph - (1 << 32), ph) > 0).astype(np.uint8)
+        truth_ok = bool(np.array_equal(dec, 1 - (a & b))) if cfg["gate"] == "NAND" else None
+    else:
+        truth_ok = bool(np.array_equal(((ph + (1 << (shift - 1))) >> shift) & ((2 << cfg["msg_bits"]) - 1), table[m]))
 
     br_ms, br_n = stages["blind_rotate"]
     br_s = br_ms / 1e3 / max(br_n, 1)
@@ -417,9 +450,11 @@ def main():
     ops = algorithmic_lane_ops(p, parts) * B
     achieved = ops / br_s
     digest = kernel_source_digest()
-    traffic = measured_traffic(digest)
+    traffic = measured_traffic(digest, args.config)
     line = {
-        "metric": METRIC,
+        "metric": METRIC if cfg["kind"] == "gate" and p["N"] == 1024 else
+                  f"{'gate' if cfg['kind'] == 'gate' else 'table-lookup'} bootstraps/sec "
+                  f"(n={p['n']},N={p['N']}) + % of VALU roofline, 1 MI355X",
         "value": value,
         "unit": "bootstraps/s",
         "n_gpus": 1,
@@ -432,11 +467,12 @@ def main():
         "vs_baseline": None,
         "dtype": "u32/f64",
         "data": "synthetic",
-        "config": {"workload": args.config, "gate": cfg["gate"], "batch": B, "n": p["n"], "N": p["N"],
-                   "l": p["l"], "bg_bit": p["bg_bit"], "ks_t": p["ks_t"], "ks_basebit": p["ks_basebit"]},
+        "config": {"workload": args.config, "gate": cfg.get("gate", "lut%d" % cfg.get("msg_bits", 0)), "batch": B,
+                   "n": p["n"], "N": p["N"], "l": p["l"], "bg_bit": p["bg_bit"], "ks_t": p["ks_t"],
+                   "ks_basebit": p["ks_basebit"]},
         "roofline": {
             "bound": "alu",
-            "kernel": "blind_rotate_kernel",
+            "kernel": "blind_rotate_kernel" if p["N"] <= 1024 else "blind_rotate_split_kernel",
             "achieved": achieved / 1e12,
             "peak": PEAK_LANE_OPS / 1e12,
             "unit": "T lane-op/s",
@@ -446,7 +482,7 @@ def main():
             "launch_ms": br_s * 1e3,
         },
         "hbm": {
-            "kernel": "blind_rotate_kernel",
+            "kernel": "blind_rotate_kernel" if p["N"] <= 1024 else "blind_rotate_split_kernel",
             "algorithmic_bytes_per_launch": algorithmic_bytes_br(p, B, parts),
             "achieved_GBps": algorithmic_bytes_br(p, B, parts) / br_s / 1e9,
             "peak_GBps": PEAK_HBM / 1e9,
@@ -463,7 +499,7 @@ def main():
                           "source": "Section 3.1 (forward/backward ReLU, forward softmax), Section 4 setup"},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, ca_h, cb_h, out)
+        line["cpu_baseline"] = cpu_baseline(cfg, ca_h, cb_h, out, tv_h)
     print(json.dumps(line), flush=True)
 
 
