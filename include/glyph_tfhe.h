@@ -27,6 +27,12 @@
  *     read secret key material.
  *   - Inputs and outputs of one server-side call must not overlap.  Concurrent
  *     calls on different streams are safe when they use different workspaces.
+ *   - A server-side call launches one-dimensional grids with one work-item per
+ *     word of its widest buffer, and a grid dimension holds at most 2^32 - 1
+ *     work-items: a call whose count times words per item exceeds 2^32 - 256
+ *     returns TFHE_EINVAL before any launch (a bootstrap call: B * (n + 1),
+ *     i.e. at most 6.8 million ciphertexts at n = 630).  Split larger batches;
+ *     the ReLU units take gate windows for this.
  */
 #ifndef GLYPH_TFHE_H
 #define GLYPH_TFHE_H
@@ -39,7 +45,8 @@ extern "C" {
 enum {
   TFHE_OK = 0,
   TFHE_EINVAL = -1,       /* bad argument: NULL pointer, negative count, unknown gate,
-                             workspace too small, misaligned pointer */
+                             workspace too small, misaligned pointer, a count too
+                             large for one launch */
   TFHE_EUNSUPPORTED = -2, /* parameter set outside what the kernels are built for */
   TFHE_ENOMEM = -3,       /* host or device allocation failed (key generation only) */
   TFHE_EHIP = -4,         /* a HIP runtime call or kernel launch failed */

@@ -2,6 +2,7 @@
 // key handles, workspace carving and kernel launches.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -55,6 +56,20 @@ namespace {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(TFHE_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// The one-dimensional launches put one work-item on each word (or sample)
+// and HIP takes at most 2^32 - 1 work-items in a grid dimension.  Every
+// server-side call bounds count * words_per_item by this before it forms
+// any product of counts, so none of them can overflow either.
+constexpr int64_t kMaxItems = (int64_t{1} << 32) - 256;
+
+int check_count(int64_t count, int64_t words_per_item, const char* what) {
+  if (count > kMaxItems / words_per_item)
+    return fail(TFHE_EINVAL, "%lld %s of %lld words each exceed the %lld words of one launch; split the call",
+                static_cast<long long>(count), what, static_cast<long long>(words_per_item),
+                static_cast<long long>(kMaxItems));
+  return TFHE_OK;
 }
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
@@ -384,6 +399,7 @@ int tfhe_lut_testvec(int32_t N, int32_t msg_bits, const uint32_t* lut, uint32_t*
 
 int64_t tfhe_workspace_bytes(const tfhe_eval_key* ek, int64_t batch) {
   if (!ek || batch < 0) return fail(TFHE_EINVAL, "bad argument to tfhe_workspace_bytes");
+  if (int rc = check_count(batch, 1, "ciphertexts")) return rc;
   return workspace_bytes(ek->p, batch);
 }
 
@@ -417,6 +433,7 @@ int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t*
                               void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.n + 1, "ciphertexts")) return rc;
   if (gate < TFHE_NAND || gate > TFHE_ORYN) return fail(TFHE_EINVAL, "unknown gate %d", gate);
   if (B == 0) return TFHE_OK;
   int rc;
@@ -430,6 +447,7 @@ int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const 
                              void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.n + 1, "ciphertexts")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(testvec, "testvec")) || (rc = check_u32(out, "out")))
@@ -443,6 +461,7 @@ int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in, co
                                  void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.n + 1, "ciphertexts")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
@@ -454,6 +473,7 @@ int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in, co
 int tfhe_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B, void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.N + 1, "samples")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
@@ -468,11 +488,13 @@ int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, in
                      void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (V < 0 || bits < 2 || bits > 64) return fail(TFHE_EINVAL, "need V >= 0 and 2 <= bits <= 64");
+  if (int rc = check_count(V, bits, "values")) return rc;
   const int64_t total = V * (bits - 1);
   if (gate_begin < 0 || gate_end < gate_begin || gate_end > total)
     return fail(TFHE_EINVAL, "gate window [%lld, %lld) outside [0, %lld)", static_cast<long long>(gate_begin),
                 static_cast<long long>(gate_end), static_cast<long long>(total));
   const int64_t B = gate_end - gate_begin;
+  if (int rc = check_count(B, ek->p.n + 1, "gates")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(x, "x")) || (rc = check_u32(y, "y"))) return rc;
@@ -491,11 +513,13 @@ int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (V < 0 || bits < 1 || bits > 64 || u_bits < 1 || u_bits > 64)
     return fail(TFHE_EINVAL, "need V >= 0, 1 <= bits <= 64 and 1 <= u_bits <= 64");
+  if (int rc = check_count(V, bits, "values")) return rc;
   const int64_t total = V * bits;
   if (gate_begin < 0 || gate_end < gate_begin || gate_end > total)
     return fail(TFHE_EINVAL, "gate window [%lld, %lld) outside [0, %lld)", static_cast<long long>(gate_begin),
                 static_cast<long long>(gate_end), static_cast<long long>(total));
   const int64_t B = gate_end - gate_begin;
+  if (int rc = check_count(B, ek->p.n + 1, "gates")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(u, "u")) || (rc = check_u32(delta, "delta")) || (rc = check_u32(out, "out"))) return rc;
@@ -531,6 +555,8 @@ int tfhe_mux_batch(const tfhe_eval_key* ek, const uint32_t* c, const uint32_t* a
                    uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_, void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  // 2B halves are bootstrapped (n + 1 words each), B sums combined (N + 1)
+  if (int rc = check_count(B, 2 * (std::max(ek->p.n, ek->p.N) + 1), "multiplexers")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(c, "c")) || (rc = check_u32(a, "a")) || (rc = check_u32(b, "b")) ||
@@ -551,6 +577,13 @@ struct MuxLutLayout {
   int64_t a_off, b_off, ws_off, total, nodes_a, nodes_b, widest;
 };
 
+// words per value of the widest launch of a multiplexer tree: its leaves,
+// out_bits * 2^(msg_bits - 1) samples of n + 1 words, which also bound the
+// bootstrapped levels' samples (n + 1 words) and sums (N + 1 words)
+static int64_t mux_lut_words(const tfhe_params& p, int32_t msg_bits, int32_t out_bits) {
+  return int64_t{out_bits} * (int64_t{1} << (msg_bits - 1)) * (std::max(p.n, p.N) + 1);
+}
+
 static MuxLutLayout mux_lut_layout(const tfhe_params& p, int64_t V, int32_t msg_bits, int32_t out_bits) {
   MuxLutLayout L{};
   const int64_t row = (p.n + 1) * 4;
@@ -568,6 +601,7 @@ static MuxLutLayout mux_lut_layout(const tfhe_params& p, int64_t V, int32_t msg_
 int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_t msg_bits, int32_t out_bits) {
   if (!ek || V < 0 || msg_bits < 1 || msg_bits > 6 || out_bits < 1 || out_bits > 32)
     return fail(TFHE_EINVAL, "bad argument to glyph_mux_lut_workspace_bytes");
+  if (int rc = check_count(V, mux_lut_words(ek->p, msg_bits, out_bits), "values")) return rc;
   return mux_lut_layout(ek->p, V, msg_bits, out_bits).total;
 }
 
@@ -577,6 +611,7 @@ int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (V < 0 || msg_bits < 1 || msg_bits > 6 || out_bits < 1 || out_bits > 32)
     return fail(TFHE_EINVAL, "need V >= 0, 1 <= msg_bits <= 6, 1 <= out_bits <= 32");
+  if (int rc = check_count(V, mux_lut_words(ek->p, msg_bits, out_bits), "values")) return rc;
   if (!table) return fail(TFHE_EINVAL, "NULL table");
   for (int k = 0; k < (1 << msg_bits); k++)
     if (out_bits < 32 && (table[k] >> out_bits) != 0)
@@ -621,6 +656,8 @@ int tfhe_pack_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* lwe, int3
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (!ek->pks) return fail(TFHE_EINVAL, "the eval key has no packing key (call tfhe_packing_key_upload)");
   if (B < 0 || Z < 1 || Z > ek->p.N) return fail(TFHE_EINVAL, "need B >= 0 and 1 <= Z <= N");
+  // B * 2N words initialised, then B blocks of 256 work-items
+  if (int rc = check_count(B, std::max(2 * ek->p.N, 256), "ciphertexts")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(lwe, "lwe")) || (rc = check_u32(out, "out"))) return rc;
@@ -633,6 +670,7 @@ int tfhe_sample_extract_batch(int32_t N, const uint32_t* trlwe, int64_t B, int32
                               void* stream) {
   if (N < 2 || N > 4096 || (N & (N - 1))) return fail(TFHE_EINVAL, "N must be a power of two in [2, 4096]");
   if (B < 0 || K < 1 || K > N) return fail(TFHE_EINVAL, "need B >= 0 and 1 <= K <= N");
+  if (int rc = check_count(B, int64_t{K} * (N + 1), "ciphertexts")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(trlwe, "trlwe")) || (rc = check_u32(out, "out"))) return rc;
@@ -641,6 +679,7 @@ int tfhe_sample_extract_batch(int32_t N, const uint32_t* trlwe, int64_t B, int32
 
 int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {
   if (dim < 1 || count < 0) return fail(TFHE_EINVAL, "need dim >= 1 and count >= 0");
+  if (int rc = check_count(count, int64_t{dim} + 1, "samples")) return rc;
   if (count == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
@@ -651,6 +690,7 @@ int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const u
                               int64_t B, void* stream) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.N, "products")) return rc;
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(d, "d")) || (rc = check_u32(b, "b")) || (rc = check_u32(c, "c"))) return rc;

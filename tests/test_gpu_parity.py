@@ -733,6 +733,52 @@ def test_workspace_too_small_is_rejected(torch):
     assert ei.value.rc == tfhe.TFHE_EINVAL
 
 
+def test_counts_too_large_for_one_launch_are_refused(torch):
+    """Every server-side call refuses, before any launch, a count whose
+    one-dimensional launch would exceed 2^32 - 256 work-items, and the size
+    queries refuse counts no call accepts.  Each call passes a NULL data
+    pointer, so a call that passed the count check would fail on it instead,
+    with another message: no call here can reach a launch."""
+    import ctypes
+
+    p = wl.CONFIGS["toy"]["params"]  # n = 64, N = 256
+    sk, ek = tfhe.tfhe_keygen_from_seed(p, 7, 0)
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    L = tfhe.lib()
+    h = ek.handle
+    most = (1 << 32) - 256
+    ws = tfhe.alloc_workspace(ek, 8)
+    wp, wb = tfhe._dptr(ws), ws.numel()
+
+    def refused(rc, what):
+        msg = L.tfhe_last_error().decode()
+        assert rc == tfhe.TFHE_EINVAL and "exceed" in msg and what in msg, (rc, msg)
+
+    B = most // 65 + 1  # n + 1 = 65 words per ciphertext
+    say(f"count limits: bootstraps of {B} ciphertexts")
+    refused(L.tfhe_gate_bootstrap_batch(h, 0, None, None, None, B, wp, wb, None), "ciphertexts")
+    refused(L.tfhe_lut_bootstrap_batch(h, None, None, None, B, wp, wb, None), "ciphertexts")
+    refused(L.tfhe_bootstrap_extract_batch(h, None, None, None, B, wp, wb, None), "ciphertexts")
+    assert L.tfhe_gate_bootstrap_batch(h, 0, None, None, None, B - 1, wp, wb, None) == tfhe.TFHE_EINVAL
+    assert "NULL" in L.tfhe_last_error().decode()  # one fewer passes the count check
+    refused(L.tfhe_keyswitch_batch(h, None, None, most // 257 + 1, None), "samples")
+    refused(L.glyph_relu_batch(h, None, None, most // 8 + 1, 8, 0, 1, wp, wb, None), "values")
+    refused(L.glyph_relu_batch(h, None, None, 10_000_000, 8, 0, most // 65 + 1, wp, wb, None), "gates")
+    refused(L.glyph_irelu_batch(h, None, 8, None, None, most // 8 + 1, 8, 0, 1, wp, wb, None), "values")
+    refused(L.glyph_irelu_batch(h, None, 8, None, None, 10_000_000, 8, 0, most // 65 + 1, wp, wb, None),
+            "gates")
+    refused(L.tfhe_mux_batch(h, None, None, None, None, most // 514 + 1, wp, wb, None), "multiplexers")
+    table = (ctypes.c_uint32 * 8)(0, 1, 2, 3, 4, 5, 6, 7)
+    V = most // (3 * 4 * 257) + 1
+    refused(L.glyph_mux_lut_batch(h, None, 3, table, 3, None, V, wp, wb, None), "values")
+    assert L.glyph_mux_lut_workspace_bytes(h, V, 3, 3) == tfhe.TFHE_EINVAL
+    assert L.glyph_mux_lut_workspace_bytes(h, V - 1, 3, 3) > 0
+    refused(L.tfhe_pack_keyswitch_batch(h, None, 1, None, most // 512 + 1, None), "ciphertexts")
+    refused(L.tfhe_negacyclic_mul_batch(h, None, None, None, most // 256 + 1, None), "products")
+    assert L.tfhe_workspace_bytes(h, most + 1) == tfhe.TFHE_EINVAL
+    assert L.tfhe_workspace_bytes(h, most) > 0
+
+
 def test_empty_and_invalid_calls(torch):
     """Empty batches are no-ops that leave the output untouched; gate windows
     outside the tensor, a missing packing key and bad table sizes are

@@ -149,3 +149,31 @@ def test_binding_checks_buffers_before_any_call():
         tfhe._dbuf(torch.zeros(7, dtype=torch.int32), 8, "x")
     with pytest.raises(ValueError, match="device tensor"):
         tfhe._dbuf(torch.zeros(8, dtype=torch.int32), 8, "x")
+
+
+MAX_ITEMS = (1 << 32) - 256  # work-items of one launch dimension the library allows
+
+
+def test_counts_too_large_for_one_launch_are_refused():
+    """The calls that take no eval key refuse, before any HIP call, a count
+    whose one-dimensional launch would exceed 2^32 - 256 work-items.  Their
+    data pointers are NULL, so a call that passed the count check fails on
+    those instead, with another message: nothing here can reach a launch."""
+    L = tfhe.lib()
+
+    def refused(rc):
+        return rc == tfhe.TFHE_EINVAL and "exceed" in L.tfhe_last_error().decode()
+
+    def null_buffer(rc):
+        return rc == tfhe.TFHE_EINVAL and "NULL" in L.tfhe_last_error().decode()
+
+    # sample extraction of all 256 coefficients at N = 256: 256 * 257 words per ciphertext
+    most = MAX_ITEMS // (256 * 257)
+    assert most == 65280
+    assert null_buffer(L.tfhe_sample_extract_batch(256, None, most, 256, None, None))
+    assert refused(L.tfhe_sample_extract_batch(256, None, most + 1, 256, None, None))
+    # NOT of LWE samples of dimension 64: 65 words each
+    most = MAX_ITEMS // 65
+    assert null_buffer(L.tfhe_not_batch(64, None, None, most, None))
+    assert refused(L.tfhe_not_batch(64, None, None, most + 1, None))
+    assert refused(L.tfhe_not_batch((1 << 31) - 1, None, None, 3, None))  # no overflow in dim + 1
