@@ -121,13 +121,28 @@ def cpu_baseline(cfg, ca, cb, gpu_out, testvec=None):
         t0 = time.perf_counter()
         ref = oracle.lut_bootstrap(keys, ca[:count], testvec)
     dt = time.perf_counter() - t0
+    # the same oracle on one thread, over the first one or two bootstraps
+    one = 2 if testvec is None else 1
+    oracle.set_threads(1)
+    try:
+        t1 = time.perf_counter()
+        if testvec is None:
+            ref1 = oracle.gate_bootstrap(keys, cfg["gate"], ca[:one], cb[:one])
+        else:
+            ref1 = oracle.lut_bootstrap(keys, ca[:one], testvec)
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_threads(threads)
     return {
         "value": count / dt, "unit": "bootstraps/s", "cores": threads, "kind": "oracle",
         "sample": f"first {count} {what} of the batch (schoolbook products, "
                   f"OpenMP over bootstraps), {dt:.1f} s wall",
         "host_cpu": host_cpu_model(),
-        "core_seconds_per_bootstrap": dt * threads / count,
-        "matches_gpu": bool(np.array_equal(ref, tfhe.to_host(gpu_out)[:count])),
+        "host_nproc": os.cpu_count(),
+        "single_thread_s_per_bootstrap": dt1 / one,
+        "single_thread_sample": f"first {one} of the same {what} on one thread, {dt1:.1f} s",
+        "matches_gpu": bool(np.array_equal(ref, tfhe.to_host(gpu_out)[:count])
+                            and np.array_equal(ref1, ref[:one])),
     }
 
 

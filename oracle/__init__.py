@@ -93,6 +93,7 @@ def _load():
                                      _u32p]),
         "oracle_not": (None, [ctypes.c_int32, _u32p, _u32p, ctypes.c_int64]),
         "oracle_threads": (ctypes.c_int, []),
+        "oracle_set_threads": (None, [ctypes.c_int]),
         "oracle_pks_words": (ctypes.c_int64, [P]),
         "oracle_packing_keygen": (None, [P, ctypes.c_uint64, _u32p, _u32p, _u32p]),
         "oracle_pack_keyswitch": (None, [P, _u32p, _u32p, ctypes.c_int32, _u32p]),
@@ -438,3 +439,8 @@ def not_gate(ct):
 
 def threads():
     return _load().oracle_threads()
+
+
+def set_threads(n: int):
+    """Threads of later oracle calls from this thread (timing only)."""
+    _load().oracle_set_threads(int(n))

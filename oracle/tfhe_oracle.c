@@ -415,6 +415,16 @@ int oracle_threads(void) {
 #endif
 }
 
+/* Threads of the calling thread's later parallel regions (n >= 1), for
+ * timing the oracle on one core; the results do not depend on it. */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* ------------------------------------------------------------------------
  * TFHE side of the cryptosystem switch (Section 3.2: step 2, functional key
  * switching from T^N to T_N[X]; step 3, SampleExtract of K coefficients;

@@ -100,6 +100,8 @@ void oracle_relu_gates(const oracle_params* p, const uint32_t* bk, const uint32_
                        int64_t count, uint32_t* out);
 void oracle_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count);
 int oracle_threads(void);
+/* Threads of the calling thread's later parallel regions (n >= 1); timing only. */
+void oracle_set_threads(int n);
 
 /* ---- TFHE side of the cryptosystem switch (Section 3.2) ---------------- */
 int64_t oracle_pks_words(const oracle_params* p);  /* n * t * (base-1) * 2 * N */

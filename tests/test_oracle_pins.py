@@ -533,3 +533,25 @@ def test_functional_bootstrap_onto_multiples_of_inverse_modulus():
     out = oracle.bootstrap_no_ks(keys, ct, tv)
     ph = oracle.phase(keys.S, out).astype(np.int64)
     assert np.array_equal(((ph * q + (1 << 31)) >> 32) % q, f[m])
+
+
+def test_results_do_not_depend_on_the_thread_count():
+    """The oracle spreads ciphertexts over OpenMP threads; each bootstrap is
+    computed by one thread from its own inputs, so one thread and all of
+    them give the same bits (the CPU baseline times both)."""
+    keys = oracle.Keys(TOY, 4246)
+    rng = np.random.default_rng(8)
+    bits = rng.integers(0, 2, (2, 12)).astype(np.uint32)
+    mu = np.where(bits == 1, 1 << 29, (1 << 32) - (1 << 29)).astype(np.uint32)  # +-1/8
+    ca = oracle.encrypt(TOY["n"], keys.s, 93, TOY["alpha_lwe"], mu[0])
+    cb = oracle.encrypt(TOY["n"], keys.s, 94, TOY["alpha_lwe"], mu[1])
+    every = oracle.gate_bootstrap(keys, "NAND", ca, cb)
+    threads = oracle.threads()
+    oracle.set_threads(1)
+    try:
+        assert oracle.threads() == 1
+        one = oracle.gate_bootstrap(keys, "NAND", ca, cb)
+    finally:
+        oracle.set_threads(threads)
+    assert oracle.threads() == threads
+    assert np.array_equal(every, one)
