@@ -144,10 +144,19 @@ def _wsbuf(ws, device):
     return _dptr(ws), ws.numel() * ws.element_size()
 
 
-def _stream(stream):
+def _stream(stream, device, *tensors):
+    """Handle of the HIP stream a call enqueues on: `stream`, else the
+    current stream of the key's device.  The device buffers handed to a
+    caller-given stream are recorded on it (torch's record_stream): once
+    Python drops one (a workspace allocated here, an input the caller lets
+    go), the caching allocator would otherwise give its memory to the next
+    allocation on another stream while the call may still be running."""
     import torch
     if stream is None:
-        stream = torch.cuda.current_stream()
+        return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+    for t in tensors:
+        if t is not None and t.is_cuda:
+            t.record_stream(stream)
     return ctypes.c_void_p(stream.cuda_stream)
 
 
@@ -297,7 +306,7 @@ def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=Non
     w = B * (n + 1)
     d = ek.device
     _check(lib().tfhe_gate_bootstrap_batch(ek.handle, g, _dbuf(ca, w, "ca", d), _dbuf(cb, w, "cb", d),
-                                           _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
+                                           _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, ca, cb, out, ws)))
     return out
 
 
@@ -307,7 +316,7 @@ def tfhe_lut_bootstrap_batch(ek: EvalKey, x, testvec, out=None, workspace=None, 
     ws = alloc_workspace(ek, B) if workspace is None else workspace
     w, d = B * (ek.params.n + 1), ek.device
     _check(lib().tfhe_lut_bootstrap_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(testvec, ek.params.N, "testvec", d),
-                                          _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
+                                          _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, x, testvec, out, ws)))
     return out
 
 
@@ -319,7 +328,7 @@ def tfhe_bootstrap_extract_batch(ek: EvalKey, x, testvec=None, out=None, workspa
     tv = _dbuf(testvec, p.N, "testvec", d) if testvec is not None else ctypes.c_void_p(0)
     _check(lib().tfhe_bootstrap_extract_batch(ek.handle, _dbuf(x, B * (p.n + 1), "x", d), tv,
                                               _dbuf(out, B * (p.N + 1), "out", d), B, *_wsbuf(ws, d),
-                                              _stream(stream)))
+                                              _stream(stream, d, x, testvec, out, ws)))
     return out
 
 
@@ -328,7 +337,7 @@ def tfhe_keyswitch_batch(ek: EvalKey, x, out=None, stream=None):
     out = _empty((B, ek.params.n + 1), ek) if out is None else out
     p, d = ek.params, ek.device
     _check(lib().tfhe_keyswitch_batch(ek.handle, _dbuf(x, B * (p.N + 1), "x", d),
-                                      _dbuf(out, B * (p.n + 1), "out", d), B, _stream(stream)))
+                                      _dbuf(out, B * (p.n + 1), "out", d), B, _stream(stream, d, x, out)))
     return out
 
 
@@ -342,7 +351,7 @@ def glyph_relu_batch(ek: EvalKey, x, bits: int, y=None, gate_begin: int = 0, gat
     ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
     w, d = V * bits * (n + 1), ek.device
     _check(lib().glyph_relu_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(y, w, "y", d), V, bits, gate_begin,
-                                  gate_end, *_wsbuf(ws, d), _stream(stream)))
+                                  gate_end, *_wsbuf(ws, d), _stream(stream, d, x, y, ws)))
     return y
 
 
@@ -359,7 +368,7 @@ def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate
     row, d = ek.params.n + 1, ek.device
     _check(lib().glyph_irelu_batch(ek.handle, _dbuf(u, V * u_bits * row, "u", d), u_bits,
                                    _dbuf(delta, V * bits * row, "delta", d), _dbuf(out, V * bits * row, "out", d),
-                                   V, bits, gate_begin, gate_end, *_wsbuf(ws, d), _stream(stream)))
+                                   V, bits, gate_begin, gate_end, *_wsbuf(ws, d), _stream(stream, d, u, delta, out, ws)))
     return out
 
 
@@ -370,7 +379,7 @@ def tfhe_mux_batch(ek: EvalKey, c, a, b, out=None, workspace=None, stream=None):
     ws = alloc_workspace(ek, 2 * B) if workspace is None else workspace
     w, d = B * (ek.params.n + 1), ek.device
     _check(lib().tfhe_mux_batch(ek.handle, _dbuf(c, w, "c", d), _dbuf(a, w, "a", d), _dbuf(b, w, "b", d),
-                                _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream)))
+                                _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, c, a, b, out, ws)))
     return out
 
 
@@ -400,7 +409,7 @@ def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspac
     row, d = ek.params.n + 1, ek.device
     _check(lib().glyph_mux_lut_batch(ek.handle, _dbuf(x, V * msg_bits * row, "x", d), msg_bits, _hptr(t), out_bits,
                                      _dbuf(out, V * out_bits * row, "out", d), V, *_wsbuf(ws, d),
-                                     _stream(stream)))
+                                     _stream(stream, d, x, out, ws)))
     return out
 
 
@@ -421,7 +430,7 @@ def tfhe_pack_keyswitch_batch(ek: EvalKey, lwe, out=None, stream=None):
     out = _empty((B, 2, ek.params.N), ek) if out is None else out
     p, d = ek.params, ek.device
     _check(lib().tfhe_pack_keyswitch_batch(ek.handle, _dbuf(lwe, B * Z * (p.n + 1), "lwe", d), Z,
-                                           _dbuf(out, B * 2 * p.N, "out", d), B, _stream(stream)))
+                                           _dbuf(out, B * 2 * p.N, "out", d), B, _stream(stream, d, lwe, out)))
     return out
 
 
@@ -432,7 +441,7 @@ def tfhe_sample_extract_batch(trlwe, K: int, out=None, stream=None):
     out = torch.empty((B, K, N + 1), dtype=torch.int32, device=trlwe.device) if out is None else out
     d = trlwe.device.index
     _check(lib().tfhe_sample_extract_batch(N, _dbuf(trlwe, B * 2 * N, "trlwe", d), B, K,
-                                           _dbuf(out, B * K * (N + 1), "out", d), _stream(stream)))
+                                           _dbuf(out, B * K * (N + 1), "out", d), _stream(stream, d, trlwe, out)))
     return out
 
 
@@ -450,7 +459,7 @@ def tfhe_not_batch(x, out=None, stream=None):
     out = torch.empty_like(x) if out is None else out
     w = count * (dim + 1)
     _check(lib().tfhe_not_batch(dim, _dbuf(x, w, "x"), _dbuf(out, w, "out", x.device.index), count,
-                                _stream(stream)))
+                                _stream(stream, x.device.index, x, out)))
     return out
 
 
@@ -460,7 +469,7 @@ def tfhe_negacyclic_mul_batch(ek: EvalKey, d, b, out=None, stream=None):
     out = torch.empty_like(b) if out is None else out
     w, dev = B * ek.params.N, ek.device
     _check(lib().tfhe_negacyclic_mul_batch(ek.handle, _dbuf(d, w, "d", dev), _dbuf(b, w, "b", dev),
-                                           _dbuf(out, w, "out", dev), B, _stream(stream)))
+                                           _dbuf(out, w, "out", dev), B, _stream(stream, dev, d, b, out)))
     return out
 
 

@@ -282,6 +282,50 @@ def test_concurrent_calls_on_two_streams(torch):
         assert np.array_equal(tfhe.to_host(outs[k]), ref[k])
 
 
+def test_buffers_given_to_a_side_stream_are_not_reused_early(torch):
+    """A buffer handed to a call on a caller-given stream is recorded on that
+    stream: when Python drops it right after the call, torch's caching
+    allocator does not give its memory to the next allocation on the default
+    stream while the side stream still has work queued, and the call's
+    result is that of the same call on the default stream."""
+    p = wl.CONFIGS["toy"]["params"]
+    sk, ek, ok = keys_for("toy", torch)
+    B = 8
+    size = tfhe.tfhe_workspace_bytes(ek, B)
+    first = torch.empty(size, dtype=torch.uint8, device="cuda:0")
+    ptr = first.data_ptr()
+    del first
+    again = torch.empty(size, dtype=torch.uint8, device="cuda:0")
+    if again.data_ptr() != ptr:
+        pytest.skip("the allocator does not hand a freed block of this size straight back")
+    del again
+    rng = np.random.default_rng(29)
+    big = 16384
+    busy = [tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 50, tfhe.encode_bits(rng.integers(0, 2, big)), k * big))
+            for k in range(2)]
+    a, b = rng.integers(0, 2, B), rng.integers(0, 2, B)
+    ca = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 51, tfhe.encode_bits(a), 0))
+    cb = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, 51, tfhe.encode_bits(b), B))
+    ref = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb))
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    say(f"side stream: {big} toy NAND gates, then {B} with a workspace dropped at once")
+    tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", *busy, stream=side)  # keeps the side stream busy
+    ws = tfhe.alloc_workspace(ek, B)
+    ptr = ws.data_ptr()
+    out = tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb, workspace=ws, stream=side)
+    del ws
+    other = torch.empty(size, dtype=torch.uint8, device="cuda:0")
+    still_busy = not side.query()
+    reused = other.data_ptr() == ptr
+    other.fill_(0xA5)  # a write on the default stream, where the workspace lived
+    torch.cuda.synchronize()
+    say(f"side stream busy at the allocation: {still_busy}; block handed back: {reused}")
+    if still_busy:
+        assert not reused
+    assert np.array_equal(tfhe.to_host(out), ref)
+
+
 def test_relu_toy_all_values(torch):
     """All 256 8-bit values through the ReLU unit on the toy parameters,
     streamed in uneven gate windows."""
