@@ -253,7 +253,9 @@ int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_
  * v in [1, 2^ks_basebit), is a TRLWE sample under S of the constant
  * polynomial v * s_i * 2^(32 - (j+1)*ks_basebit), noise alpha_bk) and add it
  * to the eval key on its device.  n * ks_t * (2^ks_basebit - 1) * 2N words
- * (124 MB at n = 630, N = 1024); a second call is a no-op. */
+ * (124 MB at n = 630, N = 1024); a second call is a no-op.  sk must be the
+ * secret key the eval key was made from (checked against a digest of the
+ * eval key's public key-switching key: TFHE_EINVAL otherwise). */
 int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek);
 
 /* Client side: copy the packing key (built on first use) to host memory,

@@ -88,6 +88,23 @@ struct DeviceGuard {
   }
 };
 
+// FNV-1a over the first 2^16 words of the key-switching key and its length:
+// keys from different seeds differ there, and the key-switching key is part
+// of the eval key, so the digest reveals nothing secret
+uint64_t key_tag(const tfhe_secret_key& sk) {
+  uint64_t h = 1469598103934665603ull;
+  auto mix = [&](uint64_t v) {
+    for (int b = 0; b < 8; b++) {
+      h ^= (v >> (8 * b)) & 0xffu;
+      h *= 1099511628211ull;
+    }
+  };
+  mix(sk.ksk.size());
+  const size_t m = std::min<size_t>(sk.ksk.size(), size_t{1} << 16);
+  for (size_t k = 0; k < m; k++) mix(sk.ksk[k]);
+  return h;
+}
+
 int check_ws(const tfhe_eval_key* ek, void* ws, int64_t ws_bytes, int64_t B) {
   if (ws == nullptr) return fail(TFHE_EINVAL, "workspace is NULL");
   if (!aligned(ws, 256)) return fail(TFHE_EINVAL, "workspace must be 256-byte aligned");
@@ -214,6 +231,7 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   ek->ksk = nullptr;
   ek->pks = nullptr;
   ek->pks_bytes = 0;
+  ek->key_tag = key_tag(*sk);
   // [n][2l][2 * parts][N/2] complex doubles
   ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
   ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
@@ -313,6 +331,8 @@ int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek) {
   if (a.n != b.n || a.N != b.N || a.l != b.l || a.bg_bit != b.bg_bit || a.ks_t != b.ks_t ||
       a.ks_basebit != b.ks_basebit || a.alpha_bk != b.alpha_bk)
     return fail(TFHE_EINVAL, "secret key and eval key have different parameters");
+  if (key_tag(*sk) != ek->key_tag)
+    return fail(TFHE_EINVAL, "the eval key was not made from this secret key");
   if (ek->pks) return TFHE_OK;
   try {
     if (sk->pks.empty()) packing_keygen_host(*sk);

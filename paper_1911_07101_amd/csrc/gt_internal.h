@@ -28,6 +28,8 @@ struct tfhe_eval_key {
   int64_t bk_bytes;
   int64_t ksk_bytes;
   int64_t pks_bytes;
+  uint64_t key_tag;  // digest of the start of the key-switching key (public material), which ties
+                     // a packing key to the secret key this eval key was made from
 };
 
 namespace gt {

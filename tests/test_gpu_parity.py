@@ -862,3 +862,7 @@ def test_empty_and_invalid_calls(torch):
     with pytest.raises(tfhe.TfheError) as ei:
         tfhe.tfhe_pack_keyswitch_batch(ek2, tfhe.to_device(np.zeros((1, 3, row), np.uint32)))
     assert ei.value.rc == tfhe.TFHE_EINVAL
+    with pytest.raises(tfhe.TfheError) as ei:  # a packing key built from another secret key
+        tfhe.tfhe_packing_key_upload(sk, ek2)
+    assert ei.value.rc == tfhe.TFHE_EINVAL and "not made from" in str(ei.value)
+    tfhe.tfhe_packing_key_upload(sk2, ek2)  # its own secret key
