@@ -98,6 +98,78 @@ def host_cpu_model() -> str:
     return platform.processor() or platform.machine()
 
 
+def parse_sclk(text: str):
+    """Current shader clock (MHz) from the driver's DPM table (sysfs
+    pp_dpm_sclk): the numbered level marked '*'; None while the GPU sleeps
+    (the 'S:' line is marked) or if no level is marked."""
+    import re
+    for line in text.splitlines():
+        m = re.match(r"\s*(\d+):\s*(\d+)\s*mhz\s*\*", line, re.I)
+        if m:
+            return int(m.group(2))
+    return None
+
+
+def sclk_path():
+    """pp_dpm_sclk of cuda:0's card (matched by PCI address), else of the
+    only card, else None."""
+    import glob
+
+    import torch
+    cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+    try:
+        pr = torch.cuda.get_device_properties(0)
+        bus = f"{pr.pci_domain_id:04x}:{pr.pci_bus_id:02x}:{pr.pci_device_id:02x}"
+        for c in cards:
+            if os.path.basename(os.path.realpath(os.path.dirname(c))).startswith(bus):
+                return c
+    except (AttributeError, RuntimeError, OSError):
+        pass
+    return cards[0] if len(cards) == 1 else None
+
+
+class ClockSampler:
+    """The GPU's shader clock over the warm-up and timed steps: a host thread
+    reads the DPM table every 10 ms.  Context for the roofline fraction, whose
+    peak assumes 2.4 GHz: boxes run this kernel at 2.0 to 2.4 GHz."""
+
+    def __init__(self, path, period=0.01):
+        import threading
+        self.path, self.period, self.samples = path, period, []
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True) if path else None
+
+    def _run(self):
+        while not self._stop.is_set():
+            try:
+                with open(self.path) as fh:
+                    v = parse_sclk(fh.read())
+            except OSError:
+                return
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self._thread:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        if self._thread:
+            self._stop.set()
+            self._thread.join()
+
+    def mhz(self, least=80):
+        """Median of the final half of the samples, or None with fewer than
+        `least` of them: the driver's figure takes more than half a second to
+        settle after the GPU wakes (a 0.4 s run read 5 % low)."""
+        if len(self.samples) < least:
+            return None
+        s = sorted(self.samples[len(self.samples) // 2:])
+        return s[len(s) // 2]
+
+
 def cpu_baseline(cfg, ca, cb, gpu_out, testvec=None):
     """The oracle on the first gates (or lookups) of the batch.  ca, cb: the
     gate inputs; for a table-lookup workload ca holds the inputs and testvec
@@ -368,7 +440,7 @@ def suite(path: str):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", default="tfhe128_nand")
     ap.add_argument("--batch", type=int, default=None, help="override the batch size")
@@ -430,21 +502,22 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    with ClockSampler(sclk_path()) as clock:
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
 
-    tfhe.tfhe_stage_timing(True)
-    tfhe.tfhe_stage_times()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev[0].record(stream)
-    for k in range(args.steps):
-        step()
-        ev[k + 1].record(stream)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+        tfhe.tfhe_stage_timing(True)
+        tfhe.tfhe_stage_times()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ev[0].record(stream)
+        for k in range(args.steps):
+            step()
+            ev[k + 1].record(stream)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
     step_ms = sorted(ev[k].elapsed_time(ev[k + 1]) for k in range(args.steps))
     stages = tfhe.tfhe_stage_times()
     tfhe.tfhe_stage_timing(False)
@@ -495,6 +568,11 @@ def main():
             "traffic": traffic,
             "ops_per_bootstrap": algorithmic_lane_ops(p, parts),
             "launch_ms": br_s * 1e3,
+            # the box's clock while the steps ran (the peak assumes 2.4 GHz)
+            "clock_mhz": clock.mhz(),
+            "clock_samples": len(clock.samples),
+            "clock_mhz_range": [min(clock.samples), max(clock.samples)] if clock.samples else None,
+            "frac_at_clock": achieved / (PEAK_LANE_OPS * clock.mhz() / 2400) if clock.mhz() else None,
         },
         "hbm": {
             "kernel": "blind_rotate_kernel" if p["N"] <= 1024 else "blind_rotate_split_kernel",

@@ -47,3 +47,18 @@ def test_algorithmic_count_matches_a_stage_by_stage_count():
         assert bench.algorithmic_lane_ops(p, 2) == _lane_ops_by_stage(p["N"], p["n"], p["l"], 2)
     # the figure the roofline is quoted on
     assert bench.algorithmic_lane_ops(wl.CONFIGS["tfhe128_nand"]["params"], 2) == 143_871_840
+
+
+def test_clock_is_read_from_the_marked_dpm_level():
+    assert bench.parse_sclk("0: 500Mhz\n1: 2362Mhz *\n2: 2400Mhz\n") == 2362
+    assert bench.parse_sclk("S: 100Mhz *\n0: 500Mhz\n1: 2400Mhz\n") is None  # asleep
+    assert bench.parse_sclk("0: 500Mhz\n1: 2400Mhz *\n") == 2400
+    assert bench.parse_sclk("") is None
+    assert bench.ClockSampler(None).mhz() is None
+
+
+def test_clock_is_the_median_of_the_final_half_of_the_samples():
+    c = bench.ClockSampler(None)
+    c.samples = [1500, 1700, 2250, 2310, 2320, 2300]  # the driver's figure ramps up first
+    assert c.mhz(least=6) == 2310
+    assert c.mhz() is None  # too few samples for the figure to have settled
