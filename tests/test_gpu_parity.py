@@ -130,6 +130,36 @@ def test_blind_rotate_extract_parity_toy(torch):
     assert np.array_equal(got, oracle.bootstrap_no_ks(ok, x, tv))
 
 
+@pytest.mark.parametrize("cfg_name", ["toy", "tfhe128_nand", "lut3_n2048"])
+def test_rotation_edges(torch, cfg_name):
+    """Degenerate rotation amounts through blind rotation and extraction, bit
+    for bit against the oracle: bodies whose switched value b is 0, 1, N - 1,
+    N, N + 1 or 2N - 1 (every b in [0, 2N) at N = 256), the rotation by
+    X^N = -1 flipping signs and by X^0 leaving the accumulator unchanged, and
+    mask words whose switched values a_i take the same edge values."""
+    p = wl.CONFIGS[cfg_name]["params"]
+    n, N = p["n"], p["N"]
+    sk, ek, ok = keys_for(cfg_name, torch)
+    rng = np.random.default_rng(31)
+    step = (1 << 32) // (2 * N)  # ms(k * step) = k
+    edges = [0, 1, 2, N - 2, N - 1, N, N + 1, N + 2, 2 * N - 2, 2 * N - 1]
+    bodies = list(range(2 * N)) if N <= 256 else edges + [int(v) for v in rng.integers(0, 2 * N, 6)]
+    # at n = 630 and N = 2048 the edge samples sit at spread rows of a batch
+    # one ragged block past a full round of the timed launch shape (blocks of
+    # 8 ciphertexts at N = 1024, 4 at N = 2048); the oracle checks those rows
+    B = {"toy": len(bodies), "tfhe128_nand": 2048 + 5, "lut3_n2048": 1024 + 3}[cfg_name]
+    rows = np.linspace(0, B - 1, len(bodies)).astype(int)
+    assert len(set(rows.tolist())) == len(bodies)
+    x = rng.integers(0, M32, (B, n + 1), dtype=np.uint64).astype(np.uint32)
+    for k, c in enumerate(rows):
+        x[c, n] = bodies[k] * step
+        for i in range(len(edges)):
+            x[c, i] = edges[(i + k) % len(edges)] * step
+    say(f"rotation edges {cfg_name} N={N} B={B}, {len(rows)} rows checked")
+    got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x)))
+    assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], oracle.gate_testvec(N)))
+
+
 # parameter sets whose transform bound needs the key in three parts: the
 # three-part blind-rotation kernels (4 points per lane) at every ring size
 THREE_PARTS = {
