@@ -228,6 +228,29 @@ def test_keyswitch_parity_toy(torch):
         assert np.array_equal(got, oracle.keyswitch(ok, x))
 
 
+@pytest.mark.parametrize("B", [4096 + 3, 8192 + 5])
+def test_keyswitch_rounding_edges(torch, B):
+    """Key switching at n = 630, N = 1024 (t = 8, base 4) in both block widths
+    (16 output columns at 4096 samples, 32 at 8192), ragged: coefficients at
+    the rounding tie (half a step of 2^-16 rounds up), just below it, at 0,
+    all digits 3, and at the wrap (2^32 - 2^15 and above round to 0), bit for
+    bit against the oracle on spread rows."""
+    p = wl.CONFIGS["tfhe128_nand"]["params"]
+    N = p["N"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    rng = np.random.default_rng(37)
+    half = 1 << 15
+    edges = [0, half, half - 1, 3 * half, (1 << 32) - half, (1 << 32) - half - 1, (1 << 32) - 1,
+             0xFFFF0000, 0x55550000, 0xAAAA8000, 0x80000000, 0x7FFF8000]
+    x = rng.integers(0, M32, (B, N + 1), dtype=np.uint64).astype(np.uint32)
+    for c in range(0, B, 7):  # every 7th sample takes the edges at every coefficient
+        x[c, :N] = np.array([edges[(i + c) % len(edges)] for i in range(N)], np.uint64).astype(np.uint32)
+    rows = np.unique(np.concatenate([np.arange(0, B, 7)[:96], np.linspace(0, B - 1, 64).astype(int)]))
+    say(f"keyswitch edges B={B}, {len(rows)} rows checked")
+    got = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, tfhe.to_device(x)))
+    assert np.array_equal(got[rows], oracle.keyswitch(ok, x[rows]))
+
+
 @pytest.mark.parametrize("ks_t,ks_basebit", [(4, 3), (16, 2), (2, 5)])
 def test_keyswitch_parity_other_digit_sizes(torch, ks_t, ks_basebit):
     """The key switch for digit shapes other than t = 8, base 4 (the kernel's
