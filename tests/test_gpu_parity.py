@@ -160,6 +160,34 @@ def test_rotation_edges(torch, cfg_name):
     assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], oracle.gate_testvec(N)))
 
 
+@pytest.mark.parametrize("cfg_name", ["tfhe128_nand", "lut3_n2048"])
+def test_decomposition_edges(torch, cfg_name):
+    """The signed gadget decomposition at its edges inside the blind rotation:
+    with a constant test polynomial c, the accumulator starts as +-c in every
+    coefficient, so the first CMux decomposes D = X^a ACC - ACC in {0, 2c, -2c}.
+    c is chosen so that 2c is 2^31 (both signs alike), a rounding tie (half a
+    step below the last digit, once and three times), every digit at Bg/2 - 1,
+    or 2^32 minus half a step (rounds to 0).  Timed launch shape, oracle-checked
+    rows, bit for bit."""
+    p = wl.CONFIGS[cfg_name]["params"]
+    n, N, l, bg = p["n"], p["N"], p["l"], p["bg_bit"]
+    L = l * bg
+    sk, ek, ok = keys_for(cfg_name, torch)
+    rng = np.random.default_rng(41)
+    step = (1 << 32) // (2 * N)
+    top_digits = ((1 << (bg - 1)) - 1) * sum(1 << (31 - j * bg) for j in range(1, l + 1))
+    cs = [1 << 30, 1 << (30 - L), 3 << (30 - L), top_digits, (1 << 31) - (1 << (30 - L))]
+    B = {"tfhe128_nand": 2048 + 5, "lut3_n2048": 1024 + 3}[cfg_name]
+    rows = np.linspace(0, B - 1, 6).astype(int)
+    for c in cs:
+        tv = np.full(N, c, np.uint32)
+        x = rng.integers(0, M32, (B, n + 1), dtype=np.uint64).astype(np.uint32)
+        x[:, n] = (rng.integers(0, 2 * N, B) * step).astype(np.uint32)
+        say(f"decomposition edges {cfg_name}: c = {c:#010x}, B={B}, {len(rows)} rows checked")
+        got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x), tfhe.to_device(tv)))
+        assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], tv)), hex(c)
+
+
 # parameter sets whose transform bound needs the key in three parts: the
 # three-part blind-rotation kernels (4 points per lane) at every ring size
 THREE_PARTS = {
