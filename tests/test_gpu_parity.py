@@ -160,6 +160,30 @@ def test_rotation_edges(torch, cfg_name):
     assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], oracle.gate_testvec(N)))
 
 
+@pytest.mark.parametrize("cfg_name", ["toy", "tfhe128_nand"])
+def test_modulus_switch_ties(torch, cfg_name):
+    """The modulus switch rounds half up: words exactly half a step of
+    2^32 / 2N above a multiple (ties, which round up), one below a tie (round
+    down), and 2^32 minus half a step (rounds to 2N, i.e. 0) in every mask
+    word and body, through blind rotation and extraction, bit for bit against
+    the oracle (timed launch shape at n = 630, oracle-checked rows)."""
+    p = wl.CONFIGS[cfg_name]["params"]
+    n, N = p["n"], p["N"]
+    sk, ek, ok = keys_for(cfg_name, torch)
+    rng = np.random.default_rng(43)
+    step = (1 << 32) // (2 * N)
+    B = {"toy": 61, "tfhe128_nand": 2048 + 5}[cfg_name]
+    rows = np.arange(B) if B < 100 else np.linspace(0, B - 1, 8).astype(int)
+    k = rng.integers(0, 2 * N, (B, n + 1))
+    kind = rng.integers(0, 3, (B, n + 1))
+    x = np.where(kind == 0, k * step + step // 2,                      # tie: rounds up to k + 1
+                 np.where(kind == 1, k * step + step // 2 - 1,         # just below: k
+                          (1 << 32) - step // 2)).astype(np.uint64).astype(np.uint32)  # wraps to 0
+    say(f"modulus switch ties {cfg_name} B={B}, {len(rows)} rows checked")
+    got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x)))
+    assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], oracle.gate_testvec(N)))
+
+
 @pytest.mark.parametrize("cfg_name", ["tfhe128_nand", "lut3_n2048"])
 def test_decomposition_edges(torch, cfg_name):
     """The signed gadget decomposition at its edges inside the blind rotation:
