@@ -241,6 +241,47 @@ def test_blind_rotate_extract_three_key_parts(torch, N):
         assert np.array_equal(got[idx], oracle.bootstrap_no_ks(ok, x[idx], tv))
 
 
+@pytest.mark.parametrize("N", [256, 512, 1024])
+@pytest.mark.parametrize("l,bg_bit", [(1, 10), (2, 9), (4, 6)])
+def test_one_wave_kernel_ring_sizes_and_gadgets(torch, N, l, bg_bit):
+    """The blind rotation with two key parts at N = 256, 512 and 1024 (N/16
+    lanes per ciphertext) for gadgets other than the default: a small batch
+    (every sample checked) and one that fills blocks of 8 waves on every CU
+    plus a ragged block (spread rows checked), with an arbitrary test
+    polynomial, bit for bit against the oracle."""
+    params = dict(n=8, N=N, l=l, bg_bit=bg_bit, ks_t=8, ks_basebit=2, alpha_lwe=2 ** -15, alpha_bk=2 ** -25)
+    assert tfhe.tfhe_transform_error_bound(params)[0] == 2
+    sk, ek, ok = keys_for(f"ring{N}_l{l}_bg{bg_bit}", torch, params=params, seed=0x1024 + N + 16 * l + bg_bit)
+    rng = np.random.default_rng(53 + N + l * bg_bit)
+    tv = rng.integers(0, M32, N, dtype=np.uint64).astype(np.uint32)
+    full = 256 * 8 * 64 // (N // 16) + 3  # 256 blocks of 8 waves, plus a ragged one
+    for B, rows in ((7, np.arange(7)), (full, np.linspace(0, full - 1, 8).astype(int))):
+        x = rng.integers(0, M32, (B, 9), dtype=np.uint64).astype(np.uint32)
+        say(f"one-wave kernel N={N} l={l} bg_bit={bg_bit} B={B}")
+        got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x), tfhe.to_device(tv)))
+        assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], tv)), B
+
+
+@pytest.mark.parametrize("l,bg_bit", [(3, 7), (1, 10), (4, 6), (2, 11), (2, 9)])
+def test_split_kernel_digit_paths(torch, l, bg_bit):
+    """The two-wave blind rotation at N = 2048 with two key parts for other
+    gadgets: digits recomputed from the accumulator for each digit (l != 2 or
+    Bg > 2^10) and the second digit kept packed from the first (l = 2,
+    Bg = 2^9), in blocks of one ciphertext (a small batch, every sample
+    checked) and of four (1027 samples, spread rows checked), with an
+    arbitrary test polynomial, bit for bit against the oracle."""
+    params = dict(n=8, N=2048, l=l, bg_bit=bg_bit, ks_t=8, ks_basebit=2, alpha_lwe=2 ** -15, alpha_bk=2 ** -25)
+    assert tfhe.tfhe_transform_error_bound(params)[0] == 2
+    sk, ek, ok = keys_for(f"split_l{l}_bg{bg_bit}", torch, params=params, seed=0x5117 + 16 * l + bg_bit)
+    rng = np.random.default_rng(47 + l * bg_bit)
+    tv = rng.integers(0, M32, 2048, dtype=np.uint64).astype(np.uint32)
+    for B, rows in ((5, np.arange(5)), (1027, np.linspace(0, 1026, 8).astype(int))):
+        x = rng.integers(0, M32, (B, 9), dtype=np.uint64).astype(np.uint32)
+        say(f"split kernel l={l} bg_bit={bg_bit} B={B}")
+        got = tfhe.to_host(tfhe.tfhe_bootstrap_extract_batch(ek, tfhe.to_device(x), tfhe.to_device(tv)))
+        assert np.array_equal(got[rows], oracle.bootstrap_no_ks(ok, x[rows], tv)), B
+
+
 def test_parameter_and_batch_limits(torch):
     """The largest LWE dimension the library accepts (n = 4096, here with the
     toy ring) and a batch of 100,003 gates (many rounds of blocks and a
