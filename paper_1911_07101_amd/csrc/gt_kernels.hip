@@ -484,9 +484,9 @@ struct BrCfg {
   static constexpr int LDS_BYTES = NC * 16 + CPB * SCR * 16 + CPB * 2 * NR * 4 + (ITW_LDS ? (NC - 1) * 16 : 0);
   static_assert(LDS_BYTES <= 160 * 1024, "block exceeds the CU's LDS");
   // compiled for two waves per SIMD (256 VGPRs per wave); blocks of at most
-  // 4 waves are launched only when each SIMD gets at most one wave, and
-  // compiled for one (the compiler may then also use accumulation registers:
-  // 256 gates 8.94 -> 8.31 ms)
+  // 4 waves run with at most one wave per SIMD (launch_br) and are compiled
+  // for one (the compiler may then also use accumulation registers: 256
+  // gates 8.94 -> 8.31 ms)
   static constexpr int MIN_WAVES = WPB <= 4 ? 1 : 2;
 };
 
@@ -1400,25 +1400,27 @@ int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t
   return launch_status("blind_rotate_split_kernel");
 }
 
-// Blocks of 8 waves when the batch fills every CU with one (or more), else
-// the largest of 4, 2, 1 waves per block that still gives every CU a block:
-// a small batch then runs one or two waves per SIMD, where its CMux chain is
-// shortest.  A ciphertext of two or four waves takes blocks of 8 waves or of
-// one ciphertext.
+// Block shape by how many blocks a CU runs at once.  Blocks of one wave are
+// compiled for one wave per SIMD, so a CU runs four side by side: a batch
+// that fits four per CU takes them (the shortest CMux chain), a larger one
+// blocks of 8 waves (two per SIMD, one block per CU, shared key reads in L1).
+// A ciphertext of two waves likewise takes blocks of one ciphertext while
+// three per CU (their LDS) hold the batch, else blocks of four.  Against the
+// largest block that still gave every CU one: 600 gates 10.31 -> 9.6 ms,
+// 1024 9.64 -> 9.30, 1500 19.55 -> 13.60 (one round of 8-wave blocks instead
+// of two of 4-wave ones), 1000 lookups at N = 2048 27.2 -> 17.0 ms.
 template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
               hipStream_t st) {
   constexpr int T = BrCfg<LOGN, S, 8>::T;
   const int64_t cus = ek->cus > 0 ? ek->cus : 256;
-  auto fills = [&](int cpb) { return (B + cpb - 1) / cpb >= cus; };
+  auto blocks = [&](int cpb) { return (B + cpb - 1) / cpb; };
   if constexpr (T <= 64) {
-    if (fills(BrCfg<LOGN, S, 8>::CPB)) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
-    if (fills(BrCfg<LOGN, S, 4>::CPB)) return launch_br_blocks<LOGN, S, 4>(ek, ws, testvec, B, st);
-    if (fills(BrCfg<LOGN, S, 2>::CPB)) return launch_br_blocks<LOGN, S, 2>(ek, ws, testvec, B, st);
-    return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
+    if (blocks(BrCfg<LOGN, S, 1>::CPB) <= 4 * cus) return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
+    return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
   } else if constexpr (T == 128) {
-    if (fills(BrSplitCfg<LOGN, S, 8>::CPB)) return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
-    return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
+    if (blocks(BrSplitCfg<LOGN, S, 2>::CPB) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
+    return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
   } else {
     return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
   }

@@ -702,11 +702,13 @@ def test_tfhe128_nand_4096(torch):
 
 
 def test_block_shapes_for_small_batches(torch):
-    """A batch too small to fill every CU with 8-wave blocks runs in blocks of
-    4, 2 or 1 waves (N = 1024) or of one ciphertext (N = 2048).  Every shape,
-    with a ragged last block, gives the same samples as the full batch, and
-    the last sample of each matches the oracle."""
-    for name, sizes in (("tfhe128_nand", (2100, 1024, 600, 200, 7)), ("lut3_n2048", (1102, 100))):
+    """A batch that four one-wave blocks per CU hold (N = 1024: up to 1024
+    gates) runs in blocks of one wave, a larger one in blocks of 8; at
+    N = 2048 up to three one-ciphertext blocks per CU (768 lookups), else
+    blocks of four ciphertexts.  Both sides of each boundary, with a ragged
+    last block, give the same samples as the full batch, and the last sample
+    of each size matches the oracle."""
+    for name, sizes in (("tfhe128_nand", (2100, 1025, 1024, 600, 7)), ("lut3_n2048", (1102, 769, 768, 100))):
         cfg = wl.CONFIGS[name]
         p = cfg["params"]
         sk, ek, ok = keys_for(name, torch)
