@@ -1408,18 +1408,31 @@ int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t
 // three per CU (their LDS) hold the batch, else blocks of four.  Against the
 // largest block that still gave every CU one: 600 gates 10.31 -> 9.6 ms,
 // 1024 9.64 -> 9.30, 1500 19.55 -> 13.60 (one round of 8-wave blocks instead
-// of two of 4-wave ones), 1000 lookups at N = 2048 27.2 -> 17.0 ms.
+// of two of 4-wave ones), 1000 lookups at N = 2048 27.2 -> 17.0 ms.  A batch
+// whose last round of 8-wave blocks would be partly filled runs that tail as
+// a second launch of one-wave blocks when four per CU hold it (2100 gates
+// 29.9 -> 24.1 ms, 3000 28.8 -> 24.2, 53,760 382.6 -> 378.6).
 template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
               hipStream_t st) {
   constexpr int T = BrCfg<LOGN, S, 8>::T;
   const int64_t cus = ek->cus > 0 ? ek->cus : 256;
-  auto blocks = [&](int cpb) { return (B + cpb - 1) / cpb; };
+  auto blocks = [&](int64_t b, int cpb) { return (b + cpb - 1) / cpb; };
   if constexpr (T <= 64) {
-    if (blocks(BrCfg<LOGN, S, 1>::CPB) <= 4 * cus) return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
-    return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
+    constexpr int C1 = BrCfg<LOGN, S, 1>::CPB;
+    if (blocks(B, C1) <= 4 * cus) return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
+    // full rounds of 8-wave blocks (one per CU); a last round that one-wave
+    // blocks hold (four per CU) runs as those instead of as a partly filled
+    // round of 8-wave blocks
+    const int64_t round = int64_t{BrCfg<LOGN, S, 8>::CPB} * cus;
+    const int64_t tail = B % round;
+    if (tail == 0 || blocks(tail, C1) > 4 * cus) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
+    const int64_t head = B - tail;
+    if (int rc = launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, head, st)) return rc;
+    const Workspace rest{ws.abar + head * (ek->p.n + 1), ws.extract + head * (ek->p.N + 1)};
+    return launch_br_blocks<LOGN, S, 1>(ek, rest, testvec, tail, st);
   } else if constexpr (T == 128) {
-    if (blocks(BrSplitCfg<LOGN, S, 2>::CPB) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
+    if (blocks(B, BrSplitCfg<LOGN, S, 2>::CPB) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
     return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
   } else {
     return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
