@@ -131,7 +131,7 @@ def sclk_path():
 class ClockSampler:
     """The GPU's shader clock over the warm-up and timed steps: a host thread
     reads the DPM table every 10 ms.  Context for the roofline fraction, whose
-    peak assumes 2.4 GHz: boxes run this kernel at 2.0 to 2.4 GHz."""
+    peak assumes 2.4 GHz: MI355X machines run this kernel at 2.0 to 2.4 GHz."""
 
     def __init__(self, path, period=0.01):
         import threading
@@ -568,7 +568,7 @@ def main():
             "traffic": traffic,
             "ops_per_bootstrap": algorithmic_lane_ops(p, parts),
             "launch_ms": br_s * 1e3,
-            # the box's clock while the steps ran (the peak assumes 2.4 GHz)
+            # the GPU's clock while the steps ran (the peak assumes 2.4 GHz)
             "clock_mhz": clock.mhz(),
             "clock_samples": len(clock.samples),
             "clock_mhz_range": [min(clock.samples), max(clock.samples)] if clock.samples else None,
