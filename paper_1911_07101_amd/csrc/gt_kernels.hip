@@ -1411,7 +1411,9 @@ int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t
 // of two of 4-wave ones), 1000 lookups at N = 2048 27.2 -> 17.0 ms.  A batch
 // whose last round of 8-wave blocks would be partly filled runs that tail as
 // a second launch of one-wave blocks when four per CU hold it (2100 gates
-// 29.9 -> 24.1 ms, 3000 28.8 -> 24.2, 53,760 382.6 -> 378.6).
+// 29.9 -> 24.1 ms, 3000 28.8 -> 24.2, 53,760 382.6 -> 378.6; lookups at
+// N = 2048 as one-ciphertext blocks, three per CU: 1102 35.6 -> 30.3 ms,
+// 8292 153.0 -> 148.9).
 template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
               hipStream_t st) {
@@ -1432,8 +1434,16 @@ int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* test
     const Workspace rest{ws.abar + head * (ek->p.n + 1), ws.extract + head * (ek->p.N + 1)};
     return launch_br_blocks<LOGN, S, 1>(ek, rest, testvec, tail, st);
   } else if constexpr (T == 128) {
-    if (blocks(B, BrSplitCfg<LOGN, S, 2>::CPB) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
-    return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
+    constexpr int C1 = BrSplitCfg<LOGN, S, 2>::CPB;
+    if (blocks(B, C1) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
+    // as above: a partly filled last round runs as one-ciphertext blocks
+    const int64_t round = int64_t{BrSplitCfg<LOGN, S, 8>::CPB} * cus;
+    const int64_t tail = B % round;
+    if (tail == 0 || blocks(tail, C1) > 3 * cus) return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
+    const int64_t head = B - tail;
+    if (int rc = launch_br_split<LOGN, S, 8>(ek, ws, testvec, head, st)) return rc;
+    const Workspace rest{ws.abar + head * (ek->p.n + 1), ws.extract + head * (ek->p.N + 1)};
+    return launch_br_split<LOGN, S, 2>(ek, rest, testvec, tail, st);
   } else {
     return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
   }
