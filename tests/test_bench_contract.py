@@ -1,9 +1,12 @@
-"""bench.py's contract, checked on the CPU: one GPU only, and the
-algorithmic operation count of the blind rotation written out by hand."""
+"""bench.py's contract: one GPU only, the algorithmic operation count of the
+blind rotation written out by hand, the clock statistic (CPU), and the
+fields of the JSON line of a short run (GPU)."""
 import math
 import os
 import subprocess
 import sys
+
+import pytest
 
 import bench
 from paper_1911_07101_amd import workloads as wl
@@ -62,3 +65,28 @@ def test_clock_is_the_median_of_the_final_half_of_the_samples():
     c.samples = [1500, 1700, 2250, 2310, 2320, 2300]  # the driver's figure ramps up first
     assert c.mhz(least=6) == 2310
     assert c.mhz() is None  # too few samples for the figure to have settled
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("config", ["tfhe128_nand", "lut3_n2048"])
+def test_bench_line_has_every_field(config):
+    """A short run of bench.py (a child process) prints one JSON line with
+    the fields its readers rely on, a roofline object against the 39.3 T
+    lane-op/s VALU peak, and outputs that decrypt to the expected bits."""
+    import json
+    print(f"[bench-contract] bench.py --config {config} --steps 2 --warmup 1", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--config", config, "--steps", "2",
+                        "--warmup", "1", "--no-cpu-baseline"], capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["higher_is_better"] is True
+    assert d["config"]["workload"] == config and d["value"] > 0 and d["truth_table_ok"] is True
+    roof = d["roofline"]
+    assert roof["bound"] == "alu" and abs(roof["peak"] - 39.3216) < 1e-9
+    assert 0 < roof["frac"] < 1 and abs(roof["frac"] - roof["achieved"] / roof["peak"]) < 1e-12
+    assert roof["clock_mhz"] is None  # too few samples in so short a run for the figure to settle
