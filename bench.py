@@ -129,9 +129,10 @@ def sclk_path():
 
 
 class ClockSampler:
-    """The GPU's shader clock over the warm-up and timed steps: a host thread
-    reads the DPM table every 10 ms.  Context for the roofline fraction, whose
-    peak assumes 2.4 GHz: MI355X machines run this kernel at 2.0 to 2.4 GHz."""
+    """The GPU's shader clock while the steps run: a host thread reads the
+    DPM table every 10 ms and keeps (time, MHz) pairs.  Context for the
+    roofline fraction, whose peak assumes 2.4 GHz: MI355X machines run this
+    kernel at 2.0 to 2.4 GHz."""
 
     def __init__(self, path, period=0.01):
         import threading
@@ -147,7 +148,7 @@ class ClockSampler:
             except OSError:
                 return
             if v is not None:
-                self.samples.append(v)
+                self.samples.append((time.perf_counter(), v))
             self._stop.wait(self.period)
 
     def __enter__(self):
@@ -160,13 +161,18 @@ class ClockSampler:
             self._stop.set()
             self._thread.join()
 
-    def mhz(self, least=80):
-        """Median of the final half of the samples, or None with fewer than
-        `least` of them: the driver's figure takes more than half a second to
-        settle after the GPU wakes (a 0.4 s run read 5 % low)."""
-        if len(self.samples) < least:
+    def window(self, t0=None, t1=None):
+        """The samples taken in [t0, t1] (open ends: all)."""
+        return [v for t, v in self.samples if (t0 is None or t >= t0) and (t1 is None or t <= t1)]
+
+    def mhz(self, t0=None, t1=None, least=5):
+        """Median of the samples taken in [t0, t1], or None with fewer than
+        `least` of them.  The driver's figure takes about half a second to
+        settle after the GPU wakes, so bench.py runs untimed steps for a
+        second before the warm-up and reads only the timed window."""
+        s = sorted(self.window(t0, t1))
+        if len(s) < least:
             return None
-        s = sorted(self.samples[len(self.samples) // 2:])
         return s[len(s) // 2]
 
 
@@ -442,6 +448,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--settle", type=float, default=1.0,
+                    help="seconds of untimed steps before the warm-up (lets the clock reading settle)")
     ap.add_argument("--config", default="tfhe128_nand")
     ap.add_argument("--batch", type=int, default=None, help="override the batch size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -503,6 +511,12 @@ def main():
         del src, dst
 
     with ClockSampler(sclk_path()) as clock:
+        # untimed steps first, so that the clock figure has settled (and the
+        # GPU left its idle state) when the timed window starts
+        t_settle = time.perf_counter()
+        while time.perf_counter() - t_settle < args.settle:
+            step()
+            torch.cuda.synchronize()
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
@@ -539,6 +553,9 @@ def main():
     achieved = ops / br_s
     digest = kernel_source_digest()
     traffic = measured_traffic(digest, args.config)
+    timed_clock = clock.window(t0, t1)
+    mhz = clock.mhz(t0, t1)
+    props = torch.cuda.get_device_properties(0)
     line = {
         "metric": METRIC if cfg["kind"] == "gate" and p["N"] == 1024 else
                   f"{'gate' if cfg['kind'] == 'gate' else 'table-lookup'} bootstraps/sec "
@@ -568,23 +585,29 @@ def main():
             "traffic": traffic,
             "ops_per_bootstrap": algorithmic_lane_ops(p, parts),
             "launch_ms": br_s * 1e3,
-            # the GPU's clock while the steps ran (the peak assumes 2.4 GHz)
-            "clock_mhz": clock.mhz(),
-            "clock_samples": len(clock.samples),
-            "clock_mhz_range": [min(clock.samples), max(clock.samples)] if clock.samples else None,
-            "frac_at_clock": achieved / (PEAK_LANE_OPS * clock.mhz() / 2400) if clock.mhz() else None,
+            # the GPU's clock during the timed steps (the peak assumes 2.4 GHz)
+            "clock_mhz": mhz,
+            "clock_samples": len(timed_clock),
+            "clock_mhz_range": [min(timed_clock), max(timed_clock)] if timed_clock else None,
+            "frac_at_clock": achieved / (PEAK_LANE_OPS * mhz / 2400) if mhz else None,
         },
         "hbm": {
             "kernel": "blind_rotate_kernel" if p["N"] <= 1024 else "blind_rotate_split_kernel",
             "algorithmic_bytes_per_launch": algorithmic_bytes_br(p, B, parts),
-            "achieved_GBps": algorithmic_bytes_br(p, B, parts) / br_s / 1e9,
+            "algorithmic_GBps": algorithmic_bytes_br(p, B, parts) / br_s / 1e9,
+            # HBM bytes from the committed rocprofv3 counters of this source
+            # (FETCH_SIZE + WRITE_SIZE, calibrated on a device copy)
+            "measured_bytes_per_launch": traffic,
+            "measured_GBps": traffic / br_s / 1e9 if traffic else None,
+            "measured_frac": traffic / br_s / PEAK_HBM if traffic else None,
             "peak_GBps": PEAK_HBM / 1e9,
         },
         "stage_ms_per_step": {k: (v[0] / max(v[1], 1)) for k, v in stages.items()},
         "truth_table_ok": truth_ok,
         "transform": {"key_parts": parts, "worst_case_error": bound},
         "kernel_source_digest": digest,
-        "device": torch.cuda.get_device_name(0),
+        "device": f"{torch.cuda.get_device_name(0)} ({getattr(props, 'gcnArchName', '?')}, "
+                  f"{props.multi_processor_count} CUs)",
         # the paper's CPU timing of the same activation path (its own TFHE
         # parameters and hardware): context, not a baseline for this metric
         "paper_context": {"relu_unit_s": 0.1, "softmax_unit_s": 3.3, "bootstraps_per_relu_unit": 7,

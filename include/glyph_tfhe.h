@@ -24,9 +24,11 @@
  *     (bootstraps, key switching, ReLU) take device pointers, enqueue work on
  *     the given HIP stream (NULL = the legacy default stream) and return
  *     without synchronising; they never allocate, copy to or from the host, or
- *     read secret key material.
- *   - Inputs and outputs of one server-side call must not overlap.  Concurrent
- *     calls on different streams are safe when they use different workspaces.
+ *     read secret key material (the stage check tfhe_debug_cmux_batch alone
+ *     uploads a caller-given key row and waits for its stream).
+ *   - Inputs, outputs and the workspace of one server-side call must not
+ *     overlap (TFHE_EINVAL otherwise).  Concurrent calls on different streams
+ *     are safe when they use different workspaces.
  *   - A server-side call launches one-dimensional grids with one work-item per
  *     word of its widest buffer, and a grid dimension holds at most 2^32 - 1
  *     work-items: a call whose count times words per item exceeds 2^32 - 256
@@ -122,23 +124,39 @@ int tfhe_transform_error_bound(const tfhe_params* params, int32_t* key_parts, do
 void tfhe_eval_key_free(tfhe_eval_key* ek);
 int tfhe_eval_key_params(const tfhe_eval_key* ek, tfhe_params* out);
 
-/* Copy keys out (host buffers; any pointer may be NULL to skip it).
- *   s [n], S [N] (0/1 words); bk [n][2l][2][N] (coefficient domain);
- *   ksk [N][ks_t][2^basebit - 1][n+1]. */
+/* Copy keys out (host buffers; any pointer may be NULL to skip it): the
+ * private keys k of Section 2 ("FHE": the user keeps them) and the public
+ * evaluation material derived from them -- the TRGSW bootstrapping key and
+ * the key-switching key of Section 3.2 -- so that a client, or a check, can
+ * recompute any step on its own.
+ *   s [n], S [N] (0/1 words); bk [n][2l][2][N] (coefficient domain, rows as
+ *   in tfhe_keygen_from_seed); ksk [N][ks_t][2^basebit - 1][n+1].
+ * Each buffer must hold the stated number of words; the call reads only the
+ * secret key handle and returns TFHE_EINVAL if it is NULL. */
 int tfhe_export_keys(const tfhe_secret_key* sk, uint32_t* s, uint32_t* S, uint32_t* bk,
                      uint32_t* ksk);
 
 /* --------------------------------------------------- client side (host) ---- */
 
-/* Fresh LWE encryptions under s of mu[0..count): ciphertext c is a pure
- * function of (key, seed, first_index + c), so a large input can be produced
- * in independent pieces.  ct: [count][n+1]. */
+/* Encryption c = E(p, k) of Section 2 ("FHE") for TFHE's LWE samples
+ * (TLWE, Section 3.2): fresh encryptions under s of the torus messages
+ * mu[0..count), each (a, <a, s> + mu + e) with a uniform and e a rounded
+ * Gaussian of deviation alpha_lwe.  Ciphertext c is a pure function of
+ * (key, seed, first_index + c), so a large input can be produced in
+ * independent pieces.  mu: [count] host, ct: [count][n+1] host, written by
+ * the call.  count = 0 is a no-op; NULL buffers or a negative count or index
+ * return TFHE_EINVAL. */
 int tfhe_encrypt_torus(const tfhe_secret_key* sk, uint64_t seed, const uint32_t* mu,
                        int64_t first_index, int64_t count, uint32_t* ct);
 
-/* Decryption phase b - <a, key> of count samples.  key_kind 0: the LWE key s
- * (samples of dimension n); 1: the TRLWE key S read as an LWE key of
- * dimension N (samples produced by SampleExtract). */
+/* Decryption p = D(c, k) of Section 2 ("FHE") up to the final rounding: the
+ * phase b - <a, key> of count LWE samples, which is the message plus the
+ * noise (a bit decrypts to true when the phase, read as a signed 32-bit
+ * value, is positive).  key_kind 0: the LWE key s, rows of n+1 words;
+ * 1: the TRLWE key S read as an LWE key of dimension N, rows of N+1 words
+ * (samples produced by SampleExtract, Section 3.2 step 3).  ct:
+ * [count][dim+1] host, phase: [count] host.  The row width is fixed by
+ * key_kind, so ct must hold count rows of that width. */
 int tfhe_decrypt_phase(const tfhe_secret_key* sk, int key_kind, const uint32_t* ct,
                        int64_t count, uint32_t* phase);
 
@@ -165,9 +183,13 @@ int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t*
                               const uint32_t* cb, uint32_t* out, int64_t B, void* workspace,
                               int64_t workspace_bytes, void* stream);
 
-/* Table-lookup (programmable) bootstrap with key switching: out[c] encrypts
- * the test polynomial's value selected by in[c]'s phase.  in, out: [B][n+1]
- * device; testvec: [N] device (see tfhe_lut_testvec). */
+/* Table-lookup (programmable) bootstrap with key switching, the TFHE table
+ * lookup of the softmax unit (Section 3.1, "Forward Softmax") and the
+ * functional bootstrapping of the cryptosystem switch (Section 3.2, steps 3
+ * and 4): out[c] encrypts the test polynomial's value selected by in[c]'s
+ * phase -- coefficient 0 of X^{-phi} testvec, phi the phase switched to
+ * Z_{2N}.  in, out: [B][n+1] device; testvec: [N] device (see
+ * tfhe_lut_testvec, tfhe_torus_testvec).  B = 0 is a no-op. */
 int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const uint32_t* testvec,
                              uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes,
                              void* stream);
@@ -295,6 +317,43 @@ int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count
  * magnitudes against a schoolbook product. */
 int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
                               uint32_t* c, int64_t B, void* stream);
+
+/* ------------------------------------------------------- stage checks ---- *
+ * Single stages of the blind rotation, run by the production kernels in
+ * their production launch shapes, so that a fault can be located in one step
+ * and any chosen input -- worst cases included -- driven through them. */
+
+/* The modulus switch of Section 3.2's bootstrapping (the first step of every
+ * gate bootstrap), after the gate's linear pre-combination (Section 3.1,
+ * gates with bootstrapping): out[c][k] = round(x[c][k] * 2N / 2^32) mod 2N,
+ * ties rounded up, where x is ca itself (gate = -1) or the combination of
+ * ca and cb for gate (a tfhe_gate value).  ca, cb: [B][n+1] device (cb is
+ * ignored for gate = -1); out: [B][n+1] device uint16 words, the layout the
+ * blind rotation reads.  B = 0 is a no-op. */
+int tfhe_debug_mod_switch_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
+                                uint16_t* out, int64_t B, void* stream);
+
+/* Device workspace in bytes of tfhe_debug_cmux_batch over B accumulators. */
+int64_t tfhe_debug_cmux_workspace_bytes(const tfhe_eval_key* ek, int64_t B);
+
+/* One CMux step of the blind rotation: the external product of a TRGSW
+ * sample by a TRLWE accumulator (Section 3.2, TRGSW x TRLWE), i.e. for every
+ * accumulator c < B
+ *   acc_out[c] = ACC + sum_r Dec(X^{abar[c]} ACC - ACC)_r * bk_row[r],  ACC = acc_in[c],
+ * with the signed gadget decomposition Dec into l digits per polynomial and
+ * the negacyclic products exact in Z_{2^32}[X]/(X^N+1).  bk_row is one row
+ * of the bootstrapping key in the coefficient domain, [2l][2][N] host words
+ * (any values: a chosen key exercises the transform's worst case); it is
+ * converted to the transform domain exactly as tfhe_eval_key_upload
+ * converts the eval key's rows.  abar: [B] device, each taken mod 2N;
+ * acc_in, acc_out: [B][2][N] device (mask polynomial, then body).  The same
+ * blind-rotation kernel as every bootstrap runs, with one CMux step, in the
+ * launch shape a bootstrap batch of B takes.  The key row is uploaded from
+ * host memory, so the call waits for the stream before returning (not for
+ * production use).  B = 0 is a no-op. */
+int tfhe_debug_cmux_batch(const tfhe_eval_key* ek, const uint32_t* bk_row, const uint32_t* abar,
+                          const uint32_t* acc_in, uint32_t* acc_out, int64_t B, void* workspace,
+                          int64_t workspace_bytes, void* stream);
 
 /* ---------------------------------------------------------- profiling ---- */
 

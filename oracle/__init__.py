@@ -73,6 +73,7 @@ def _load():
         "oracle_rotate": (None, [ctypes.c_int32, _u32p, ctypes.c_uint32, _u32p]),
         "oracle_decompose": (None, [ctypes.c_int32, ctypes.c_int32, ctypes.c_uint32, _i32p]),
         "oracle_mod_switch": (ctypes.c_uint32, [ctypes.c_uint32, ctypes.c_int32]),
+        "oracle_mod_switch_batch": (None, [_u32p, ctypes.c_int64, ctypes.c_int32, _u32p]),
         "oracle_bk_words": (ctypes.c_int64, [P]),
         "oracle_ksk_words": (ctypes.c_int64, [P]),
         "oracle_keygen": (None, [P, ctypes.c_uint64, _u32p, _u32p, _u32p, _u32p]),
@@ -169,6 +170,14 @@ def mod_switch(x, N):
     return _load().oracle_mod_switch(x, N)
 
 
+def mod_switch_array(x, N):
+    """mod_switch of every word of x (any shape)."""
+    x = np.ascontiguousarray(x, dtype=np.uint32)
+    out = np.zeros_like(x)
+    _load().oracle_mod_switch_batch(_u32(x), x.size, N, _u32(out))
+    return out
+
+
 class Keys:
     """Secret and evaluation keys produced by oracle_keygen."""
 
@@ -243,6 +252,17 @@ def cmux(keys: Keys, i, abar, acc):
     acc = np.array(acc, dtype=np.uint32).ravel()
     bk_i = np.ascontiguousarray(keys.bk_view()[i]).ravel()
     _load().oracle_cmux(ctypes.byref(p), _u32(bk_i), abar, _u32(acc))
+    return acc.reshape(2, p.N)
+
+
+def cmux_row(p, bk_row, abar, acc):
+    """One CMux with a given key row bk_row ([2l][2][N] words, coefficient
+    domain) on the accumulator acc ([2][N]) rotated by abar."""
+    p = as_params(p)
+    acc = np.array(acc, dtype=np.uint32).ravel()
+    bk_row = np.ascontiguousarray(bk_row, dtype=np.uint32).ravel()
+    assert bk_row.size == 2 * p.l * 2 * p.N and acc.size == 2 * p.N
+    _load().oracle_cmux(ctypes.byref(p), _u32(bk_row), abar, _u32(acc))
     return acc.reshape(2, p.N)
 
 

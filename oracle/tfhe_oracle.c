@@ -114,6 +114,11 @@ uint32_t oracle_mod_switch(uint32_t x, int32_t N) {
   return (uint32_t)(v % twoN);
 }
 
+/* oracle_mod_switch of count words (a loop, for batches) */
+void oracle_mod_switch_batch(const uint32_t* x, int64_t count, int32_t N, uint32_t* out) {
+  for (int64_t k = 0; k < count; k++) out[k] = oracle_mod_switch(x[k], N);
+}
+
 /* ------------------------------------------------------------------------
  * Keys
  * ---------------------------------------------------------------------- */

@@ -64,6 +64,7 @@ void oracle_negacyclic_mul(int32_t N, const uint32_t* a, const uint32_t* b, uint
 void oracle_rotate(int32_t N, const uint32_t* p, uint32_t e, uint32_t* out);
 void oracle_decompose(int32_t l, int32_t bg_bit, uint32_t x, int32_t* digits);
 uint32_t oracle_mod_switch(uint32_t x, int32_t N);
+void oracle_mod_switch_batch(const uint32_t* x, int64_t count, int32_t N, uint32_t* out);
 
 /* ---- keys, encryption, decryption ------------------------------------ */
 int64_t oracle_bk_words(const oracle_params* p);   /* n * 2l * 2 * N */

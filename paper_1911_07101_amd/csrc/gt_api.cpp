@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <initializer_list>
 #include <mutex>
 #include <new>
 #include <vector>
@@ -170,6 +171,36 @@ int check_u32(const void* p, const char* name) {
   if (!aligned(p, 4)) return fail(TFHE_EINVAL, "%s is not 4-byte aligned", name);
   return TFHE_OK;
 }
+
+// One device buffer of a call, [p, p + bytes).
+struct Span {
+  const void* p;
+  int64_t bytes;
+  const char* name;
+};
+
+bool overlap(const Span& a, const Span& b) {
+  if (a.p == nullptr || b.p == nullptr || a.bytes <= 0 || b.bytes <= 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + static_cast<uintptr_t>(b.bytes) && b0 < a0 + static_cast<uintptr_t>(a.bytes);
+}
+
+// Inputs, outputs and workspace of one call must not overlap: the kernels
+// read inputs of some samples after they have written outputs of others
+// (a ReLU window, for instance, writes the sign words of values that the
+// next window's gates still read).  Every written buffer (`out`) is checked
+// against every other buffer of the call.
+int check_disjoint(std::initializer_list<Span> in, std::initializer_list<Span> out) {
+  for (const Span* o = out.begin(); o != out.end(); ++o) {
+    for (const Span& i : in)
+      if (overlap(*o, i)) return fail(TFHE_EINVAL, "%s overlaps %s", o->name, i.name);
+    for (const Span* o2 = o + 1; o2 != out.end(); ++o2)
+      if (overlap(*o, *o2)) return fail(TFHE_EINVAL, "%s overlaps %s", o->name, o2->name);
+  }
+  return TFHE_OK;
+}
+
+int64_t lwe_bytes(int64_t count, int32_t dim) { return count * (int64_t{dim} + 1) * 4; }
 
 }  // namespace
 
@@ -458,6 +489,10 @@ int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t*
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(ca, "ca")) || (rc = check_u32(cb, "cb")) || (rc = check_u32(out, "out"))) return rc;
+  const int64_t w = lwe_bytes(B, ek->p.n);
+  if ((rc = check_disjoint({{ca, w, "ca"}, {cb, w, "cb"}},
+                           {{out, w, "out"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
+    return rc;
   PrepArgs a{kModeGate, gate, ca, cb, B, 0, 0};
   return bootstrap_common(ek, a, nullptr, out, kModeGate, workspace, workspace_bytes_, stream, true);
 }
@@ -471,6 +506,10 @@ int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const 
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(testvec, "testvec")) || (rc = check_u32(out, "out")))
+    return rc;
+  const int64_t w = lwe_bytes(B, ek->p.n);
+  if ((rc = check_disjoint({{in, w, "in"}, {testvec, int64_t{ek->p.N} * 4, "testvec"}},
+                           {{out, w, "out"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
     return rc;
   PrepArgs a{kModePlain, 0, in, nullptr, B, 0, 0};
   return bootstrap_common(ek, a, testvec, out, kModePlain, workspace, workspace_bytes_, stream, true);
@@ -486,6 +525,9 @@ int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in, co
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
   if (testvec && !aligned(testvec, 4)) return fail(TFHE_EINVAL, "testvec is not 4-byte aligned");
+  if ((rc = check_disjoint({{in, lwe_bytes(B, ek->p.n), "in"}, {testvec, int64_t{ek->p.N} * 4, "testvec"}},
+                           {{out, lwe_bytes(B, ek->p.N), "out"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
+    return rc;
   PrepArgs a{kModePlain, 0, in, nullptr, B, 0, 0};
   return bootstrap_common(ek, a, testvec, out, kModePlain, workspace, workspace_bytes_, stream, false);
 }
@@ -497,6 +539,7 @@ int tfhe_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* 
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
+  if ((rc = check_disjoint({{in, lwe_bytes(B, ek->p.N), "in"}}, {{out, lwe_bytes(B, ek->p.n), "out"}}))) return rc;
   DeviceGuard g(ek->device);
   if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
   StageScope sc(2, stream);
@@ -518,6 +561,9 @@ int glyph_relu_batch(const tfhe_eval_key* ek, const uint32_t* x, uint32_t* y, in
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(x, "x")) || (rc = check_u32(y, "y"))) return rc;
+  const int64_t w = lwe_bytes(V * bits, ek->p.n);
+  if ((rc = check_disjoint({{x, w, "x"}}, {{y, w, "y"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
+    return rc;
   PrepArgs a{kModeRelu, TFHE_ANDNY, x, nullptr, B, bits, gate_begin};
   rc = bootstrap_common(ek, a, nullptr, y, kModeRelu, workspace, workspace_bytes_, stream, true);
   if (rc) return rc;
@@ -543,6 +589,10 @@ int glyph_irelu_batch(const tfhe_eval_key* ek, const uint32_t* u, int32_t u_bits
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(u, "u")) || (rc = check_u32(delta, "delta")) || (rc = check_u32(out, "out"))) return rc;
+  const int64_t w = lwe_bytes(V * bits, ek->p.n);
+  if ((rc = check_disjoint({{u, lwe_bytes(V * u_bits, ek->p.n), "u"}, {delta, w, "delta"}},
+                           {{out, w, "out"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
+    return rc;
   PrepArgs a{kModeIRelu, TFHE_ANDNY, u, delta, B, bits, gate_begin, u_bits};
   return bootstrap_common(ek, a, nullptr, out, kModeIRelu, workspace, workspace_bytes_, stream, true);
 }
@@ -581,6 +631,10 @@ int tfhe_mux_batch(const tfhe_eval_key* ek, const uint32_t* c, const uint32_t* a
   int rc;
   if ((rc = check_u32(c, "c")) || (rc = check_u32(a, "a")) || (rc = check_u32(b, "b")) ||
       (rc = check_u32(out, "out")))
+    return rc;
+  const int64_t w = lwe_bytes(B, ek->p.n);
+  if ((rc = check_disjoint({{c, w, "c"}, {a, w, "a"}, {b, w, "b"}},
+                           {{out, w, "out"}, {workspace, workspace_bytes(ek->p, 2 * B), "workspace"}})))
     return rc;
   PrepArgs pa{};
   pa.mode = kModeMux;
@@ -645,6 +699,9 @@ int glyph_mux_lut_batch(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_
   if (workspace_bytes_ < L.total)
     return fail(TFHE_EINVAL, "workspace of %lld bytes is smaller than the %lld bytes needed",
                 static_cast<long long>(workspace_bytes_), static_cast<long long>(L.total));
+  if ((rc = check_disjoint({{x, lwe_bytes(V * msg_bits, ek->p.n), "x"}},
+                           {{out, lwe_bytes(V * out_bits, ek->p.n), "out"}, {workspace, L.total, "workspace"}})))
+    return rc;
   char* base = static_cast<char*>(workspace);
   uint32_t* nodes[2] = {reinterpret_cast<uint32_t*>(base + L.a_off), reinterpret_cast<uint32_t*>(base + L.b_off)};
   {
@@ -681,6 +738,8 @@ int tfhe_pack_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* lwe, int3
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(lwe, "lwe")) || (rc = check_u32(out, "out"))) return rc;
+  if ((rc = check_disjoint({{lwe, lwe_bytes(B * Z, ek->p.n), "lwe"}}, {{out, B * 2 * ek->p.N * 4, "out"}})))
+    return rc;
   DeviceGuard g(ek->device);
   if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
   return launch_pack_keyswitch(ek, lwe, Z, out, B, stream);
@@ -694,6 +753,7 @@ int tfhe_sample_extract_batch(int32_t N, const uint32_t* trlwe, int64_t B, int32
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(trlwe, "trlwe")) || (rc = check_u32(out, "out"))) return rc;
+  if ((rc = check_disjoint({{trlwe, B * 2 * N * 4, "trlwe"}}, {{out, lwe_bytes(B * K, N), "out"}}))) return rc;
   return launch_sample_extract(N, trlwe, B, K, out, stream);
 }
 
@@ -703,6 +763,7 @@ int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count
   if (count == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(in, "in")) || (rc = check_u32(out, "out"))) return rc;
+  if ((rc = check_disjoint({{in, lwe_bytes(count, dim), "in"}}, {{out, lwe_bytes(count, dim), "out"}}))) return rc;
   return launch_not(dim, in, out, count, stream);
 }
 
@@ -714,9 +775,96 @@ int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const u
   if (B == 0) return TFHE_OK;
   int rc;
   if ((rc = check_u32(d, "d")) || (rc = check_u32(b, "b")) || (rc = check_u32(c, "c"))) return rc;
+  const int64_t w = B * ek->p.N * 4;
+  if ((rc = check_disjoint({{d, w, "d"}, {b, w, "b"}}, {{c, w, "c"}}))) return rc;
   DeviceGuard g(ek->device);
   if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
   return launch_negacyclic_mul(ek, d, b, c, B, stream);
+}
+
+int tfhe_debug_mod_switch_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
+                                uint16_t* out, int64_t B, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, ek->p.n + 1, "samples")) return rc;
+  if (gate < -1 || gate > TFHE_ORYN) return fail(TFHE_EINVAL, "gate %d is neither -1 nor a gate", gate);
+  if (B == 0) return TFHE_OK;
+  int rc;
+  if ((rc = check_u32(ca, "ca")) || (gate >= 0 && (rc = check_u32(cb, "cb")))) return rc;
+  if (out == nullptr || !aligned(out, 2)) return fail(TFHE_EINVAL, "out is NULL or not 2-byte aligned");
+  const int64_t w = lwe_bytes(B, ek->p.n);
+  if ((rc = check_disjoint({{ca, w, "ca"}, {gate >= 0 ? cb : nullptr, w, "cb"}}, {{out, w / 2, "out"}}))) return rc;
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  PrepArgs a{gate < 0 ? kModePlain : kModeGate, gate < 0 ? 0 : gate, ca, gate < 0 ? nullptr : cb, B, 0, 0};
+  Workspace ws{out, nullptr};
+  StageScope sc(0, stream);
+  return launch_prep(ek, a, ws, stream);
+}
+
+// workspace of tfhe_debug_cmux_batch: the key row in the transform domain,
+// then the modulus-switched inputs [B][2] u16
+static int64_t debug_cmux_key_bytes(const tfhe_eval_key* ek) {
+  const int64_t b = int64_t{2} * ek->p.l * 2 * ek->parts * (ek->p.N / 2) * 16;
+  return (b + 255) / 256 * 256;
+}
+
+int64_t tfhe_debug_cmux_workspace_bytes(const tfhe_eval_key* ek, int64_t B) {
+  if (!ek || B < 0) return fail(TFHE_EINVAL, "bad argument to tfhe_debug_cmux_workspace_bytes");
+  if (int rc = check_count(B, 2 * int64_t{ek->p.N}, "accumulators")) return rc;
+  return debug_cmux_key_bytes(ek) + (B * 4 + 255) / 256 * 256;
+}
+
+int tfhe_debug_cmux_batch(const tfhe_eval_key* ek, const uint32_t* bk_row, const uint32_t* abar,
+                          const uint32_t* acc_in, uint32_t* acc_out, int64_t B, void* workspace,
+                          int64_t workspace_bytes_, void* stream) {
+  if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
+  if (B < 0) return fail(TFHE_EINVAL, "negative batch");
+  if (int rc = check_count(B, 2 * int64_t{ek->p.N}, "accumulators")) return rc;
+  if (B == 0) return TFHE_OK;
+  if (!bk_row) return fail(TFHE_EINVAL, "bk_row is NULL");
+  int rc;
+  if ((rc = check_u32(abar, "abar")) || (rc = check_u32(acc_in, "acc_in")) || (rc = check_u32(acc_out, "acc_out")))
+    return rc;
+  if (!workspace || !aligned(workspace, 256)) return fail(TFHE_EINVAL, "workspace is NULL or not 256-byte aligned");
+  const int64_t need = tfhe_debug_cmux_workspace_bytes(ek, B);
+  if (workspace_bytes_ < need)
+    return fail(TFHE_EINVAL, "workspace of %lld bytes is smaller than the %lld bytes needed",
+                static_cast<long long>(workspace_bytes_), static_cast<long long>(need));
+  const int64_t acc_bytes = B * 2 * ek->p.N * 4;
+  if ((rc = check_disjoint({{abar, B * 4, "abar"}, {acc_in, acc_bytes, "acc_in"}},
+                           {{acc_out, acc_bytes, "acc_out"}, {workspace, need, "workspace"}})))
+    return rc;
+  // the key row in the transform domain, as the eval key's rows are made
+  tfhe_params p1 = ek->p;
+  p1.n = 1;
+  std::vector<double> row;
+  try {
+    row.resize(static_cast<size_t>(debug_cmux_key_bytes(ek) / 8));
+  } catch (const std::bad_alloc&) {
+    return fail(TFHE_ENOMEM, "host allocation failed for the key row");
+  }
+  bk_to_transform_host(p1, ek->parts, bk_row, row.data());
+  DeviceGuard g(ek->device);
+  if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* base = static_cast<char*>(workspace);
+  uint16_t* ab = reinterpret_cast<uint16_t*>(base + debug_cmux_key_bytes(ek));
+  hipError_t e = hipMemcpyAsync(base, row.data(), row.size() * 8, hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(e, "copy key row");
+  if ((rc = launch_cmux_abar(ek, abar, B, ab, stream))) return rc;
+  BrIo io;
+  io.acc_in = acc_in;
+  io.acc_out = acc_out;
+  io.bk = reinterpret_cast<const double*>(base);
+  io.n = 1;
+  {
+    StageScope sc(1, stream);
+    if ((rc = launch_blind_rotate(ek, Workspace{ab, nullptr}, nullptr, B, stream, &io))) return rc;
+  }
+  // the host copy of the key row must outlive the upload
+  e = hipStreamSynchronize(st);
+  return e == hipSuccess ? TFHE_OK : hip_fail(e, "stage check");
 }
 
 int tfhe_stage_timing(int enable) {

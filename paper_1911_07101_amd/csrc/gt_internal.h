@@ -93,14 +93,28 @@ struct PrepArgs {
   int32_t level = 0;          // mux tree: selector bit of this level
 };
 
+// Stage-check inputs and outputs of the blind rotation (all NULL / 0 on the
+// production path): the same kernels, in the same launch shapes, then start
+// from the caller's accumulators, run `n` CMux steps over the given
+// transform-domain key rows, and write the whole accumulators back instead
+// of their SampleExtract.
+struct BrIo {
+  const uint32_t* acc_in = nullptr;  // [B][2][N] accumulators in place of (0, X^{-bbar} v)
+  uint32_t* acc_out = nullptr;       // [B][2][N] final accumulators in place of SampleExtract
+  const double* bk = nullptr;        // transform-domain key rows in place of the eval key's
+  int n = 0;                         // CMux steps in place of the LWE dimension
+};
+
 int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws, void* stream);
 int launch_blind_rotate(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec,
-                        int64_t B, void* stream);
+                        int64_t B, void* stream, const BrIo* io = nullptr);
 int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B,
                      int mode, int32_t bits, int64_t gate_begin, void* stream);
 int launch_relu_sign(const tfhe_eval_key* ek, uint32_t* y, int32_t bits, int64_t v_begin,
                      int64_t v_end, void* stream);
 int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream);
+// abar[2c] = a[c] mod 2N, abar[2c + 1] = 0 for c < B (inputs of a one-CMux stage check)
+int launch_cmux_abar(const tfhe_eval_key* ek, const uint32_t* a, int64_t B, uint16_t* abar, void* stream);
 // ext[e] += ext[M + e] + (0, 1/8) for e < M (the multiplexer's OR of its halves)
 int launch_mux_combine(const tfhe_eval_key* ek, uint32_t* ext, int64_t M, void* stream);
 // first level of a multiplexer tree over constant leaves table[k]: node

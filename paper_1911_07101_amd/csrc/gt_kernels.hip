@@ -519,7 +519,7 @@ template <int LOGN, int S, int WPB>
 __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB>::MIN_WAVES)) void blind_rotate_kernel(
     const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
-    int64_t B) {
+    int64_t B, const uint32_t* __restrict__ acc_in, uint32_t* __restrict__ acc_out) {
   using C = BrCfg<LOGN, S, WPB>;
   using Lay = typename C::Lay;
   constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
@@ -552,8 +552,20 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
   uint32_t* acc_b = acc_a + NR;
   const uint16_t* ab = abar + c * (n + 1);
 
-  // ACC = (0, X^{-bbar} v); thread t owns ring coefficients t + T*e and t + T*e + NR/2
-  {
+  // ACC = (0, X^{-bbar} v); thread t owns ring coefficients t + T*e and t + T*e + NR/2.
+  // A stage check (acc_in given) starts from the caller's accumulator instead.
+  if (acc_in != nullptr) {
+    const uint32_t* src = acc_in + c * 2 * NR;
+#pragma unroll
+    for (int e = 0; e < E; e++)
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const int j = t + T * e + h * NC;
+        acc_a[j] = src[j];
+        acc_b[j] = src[NR + j];
+      }
+    poly_sync<T>();
+  } else {
     const uint32_t bbar = ab[n];
     const uint32_t e0 = (2u * NR - bbar) & (2u * NR - 1);
 #pragma unroll
@@ -679,8 +691,21 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
     poly_sync<T>();
   }
 
-  // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0)
-  if (active) {
+  // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0), or for a
+  // stage check (acc_out given) the whole accumulator
+  if (active && acc_out != nullptr) {
+    uint32_t* dst = acc_out + c * 2 * NR;
+    int t_x = t;
+    asm volatile("" : "+v"(t_x));
+#pragma unroll
+    for (int e = 0; e < E; e++)
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const int j = t_x + T * e + h * NC;
+        dst[j] = acc_a[j];
+        dst[NR + j] = acc_b[j];
+      }
+  } else if (active) {
     uint32_t* out = extract + c * (NR + 1);
     int t_x = t;  // hidden so that no coefficient position stays live over the CMux loop
     asm volatile("" : "+v"(t_x));
@@ -729,7 +754,7 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
                              (BrSplitCfg<LOGN, S, WPB>::MIN_WAVES)) void blind_rotate_split_kernel(
     const double2* __restrict__ bk, const double2* __restrict__ tw_g, const uint16_t* __restrict__ abar,
     const uint32_t* __restrict__ testvec, uint32_t* __restrict__ extract, int n, int l, int bg_bit,
-    int64_t B) {
+    int64_t B, const uint32_t* __restrict__ acc_in, uint32_t* __restrict__ acc_out) {
   using C = BrSplitCfg<LOGN, S, WPB>;
   using Sub = typename C::Sub;
   constexpr int NR = C::NR, NC = C::NC, HN = C::HN, E = C::E, CPB = C::CPB, O = C::O;
@@ -764,8 +789,14 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
   const double2 tw1 = tw_g[1];
   const double2 split_w = h ? make_double2(-tw1.x, -tw1.y) : tw1;
 
-  // ACC = (0, X^{-bbar} v)
-  {
+  // ACC = (0, X^{-bbar} v), or for a stage check (acc_in given) the caller's accumulator
+  if (acc_in != nullptr) {
+    const uint32_t* src = acc_in + c * 2 * NR;
+    for (int j = tc; j < NR; j += 128) {
+      acc_a[j] = src[j];
+      acc_b[j] = src[NR + j];
+    }
+  } else {
     const uint32_t bbar = ab[n];
     const uint32_t e0 = (2u * NR - bbar) & (2u * NR - 1);
     for (int j = tc; j < NR; j += 128) {
@@ -974,8 +1005,15 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
     __syncthreads();
   }
 
-  // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0)
-  if (active) {
+  // SampleExtract of coefficient 0: (A_0, -A_{N-1}, ..., -A_1, B_0), or for a
+  // stage check (acc_out given) the whole accumulator
+  if (active && acc_out != nullptr) {
+    uint32_t* dst = acc_out + c * 2 * NR;
+    for (int j = tc; j < NR; j += 128) {
+      dst[j] = acc_a[j];
+      dst[NR + j] = acc_b[j];
+    }
+  } else if (active) {
     uint32_t* out = extract + c * (NR + 1);
     for (int j = tc; j < NR; j += 128) out[j] = j == 0 ? acc_a[0] : 0u - acc_a[NR - j];
     if (tc == 0) out[NR] = acc_b[0];
@@ -1212,6 +1250,15 @@ __global__ __launch_bounds__(256) void relu_sign_kernel(uint32_t* __restrict__ y
   y[(v * bits + bits - 1) * (n + 1) + k] = k == n ? 0u - kMu : 0u;
 }
 
+// modulus-switched inputs of a one-CMux stage check: row c is (abar[c] mod 2N, 0)
+__global__ __launch_bounds__(256) void cmux_abar_kernel(const uint32_t* __restrict__ a, int N, int64_t B,
+                                                        uint16_t* __restrict__ abar) {
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (c >= B) return;
+  abar[2 * c] = static_cast<uint16_t>(a[c] & static_cast<uint32_t>(2 * N - 1));
+  abar[2 * c + 1] = 0;
+}
+
 __global__ __launch_bounds__(256) void not_kernel(const uint32_t* __restrict__ in,
                                                   uint32_t* __restrict__ out, int64_t words) {
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
@@ -1377,27 +1424,43 @@ inline int launch_status(const char* what) {
   return TFHE_OK;
 }
 
+// key rows and CMux count of a launch: the eval key's, or a stage check's
+inline const double2* br_key(const tfhe_eval_key* ek, const BrIo& io) {
+  return reinterpret_cast<const double2*>(io.bk ? io.bk : ek->bk_fft);
+}
+inline int br_steps(const tfhe_eval_key* ek, const BrIo& io) { return io.bk ? io.n : ek->p.n; }
+
 template <int LOGN, int S, int WPB>
 int launch_br_blocks(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
-                     hipStream_t st) {
+                     hipStream_t st, const BrIo& io) {
   using C = BrCfg<LOGN, S, WPB>;
   const int64_t blocks = (B + C::CPB - 1) / C::CPB;
   hipLaunchKernelGGL((blind_rotate_kernel<LOGN, S, WPB>), dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS),
-                     0, st, reinterpret_cast<const double2*>(ek->bk_fft), reinterpret_cast<const double2*>(ek->tw),
-                     ws.abar, testvec, ws.extract, ek->p.n, ek->p.l, ek->p.bg_bit, B);
+                     0, st, br_key(ek, io), reinterpret_cast<const double2*>(ek->tw), ws.abar, testvec,
+                     ws.extract, br_steps(ek, io), ek->p.l, ek->p.bg_bit, B, io.acc_in, io.acc_out);
   return launch_status("blind_rotate_kernel");
 }
 
 template <int LOGN, int S, int WPB>
 int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
-                    hipStream_t st) {
+                    hipStream_t st, const BrIo& io) {
   using C = BrSplitCfg<LOGN, S, WPB>;
   const int64_t blocks = (B + C::CPB - 1) / C::CPB;
   hipLaunchKernelGGL((blind_rotate_split_kernel<LOGN, S, WPB>), dim3(static_cast<unsigned>(blocks)),
-                     dim3(C::THREADS), 0, st, reinterpret_cast<const double2*>(ek->bk_fft),
-                     reinterpret_cast<const double2*>(ek->tw), ws.abar, testvec, ws.extract, ek->p.n, ek->p.l,
-                     ek->p.bg_bit, B);
+                     dim3(C::THREADS), 0, st, br_key(ek, io), reinterpret_cast<const double2*>(ek->tw), ws.abar,
+                     testvec, ws.extract, br_steps(ek, io), ek->p.l, ek->p.bg_bit, B, io.acc_in, io.acc_out);
   return launch_status("blind_rotate_split_kernel");
+}
+
+// the part of a launch's buffers after its first `head` ciphertexts
+inline Workspace ws_tail(const tfhe_eval_key* ek, const Workspace& ws, const BrIo& io, int64_t head) {
+  return Workspace{ws.abar + head * (br_steps(ek, io) + 1), ws.extract + head * (ek->p.N + 1)};
+}
+inline BrIo io_tail(const tfhe_eval_key* ek, const BrIo& io, int64_t head) {
+  BrIo r = io;
+  if (r.acc_in) r.acc_in += head * 2 * ek->p.N;
+  if (r.acc_out) r.acc_out += head * 2 * ek->p.N;
+  return r;
 }
 
 // Block shape by how many blocks a CU runs at once.  Blocks of one wave are
@@ -1416,36 +1479,34 @@ int launch_br_split(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t
 // 8292 153.0 -> 148.9).
 template <int LOGN, int S>
 int launch_br(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec, int64_t B,
-              hipStream_t st) {
+              hipStream_t st, const BrIo& io) {
   constexpr int T = BrCfg<LOGN, S, 8>::T;
   const int64_t cus = ek->cus > 0 ? ek->cus : 256;
   auto blocks = [&](int64_t b, int cpb) { return (b + cpb - 1) / cpb; };
   if constexpr (T <= 64) {
     constexpr int C1 = BrCfg<LOGN, S, 1>::CPB;
-    if (blocks(B, C1) <= 4 * cus) return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st);
+    if (blocks(B, C1) <= 4 * cus) return launch_br_blocks<LOGN, S, 1>(ek, ws, testvec, B, st, io);
     // full rounds of 8-wave blocks (one per CU); a last round that one-wave
     // blocks hold (four per CU) runs as those instead of as a partly filled
     // round of 8-wave blocks
     const int64_t round = int64_t{BrCfg<LOGN, S, 8>::CPB} * cus;
     const int64_t tail = B % round;
-    if (tail == 0 || blocks(tail, C1) > 4 * cus) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st);
+    if (tail == 0 || blocks(tail, C1) > 4 * cus) return launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, B, st, io);
     const int64_t head = B - tail;
-    if (int rc = launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, head, st)) return rc;
-    const Workspace rest{ws.abar + head * (ek->p.n + 1), ws.extract + head * (ek->p.N + 1)};
-    return launch_br_blocks<LOGN, S, 1>(ek, rest, testvec, tail, st);
+    if (int rc = launch_br_blocks<LOGN, S, 8>(ek, ws, testvec, head, st, io)) return rc;
+    return launch_br_blocks<LOGN, S, 1>(ek, ws_tail(ek, ws, io, head), testvec, tail, st, io_tail(ek, io, head));
   } else if constexpr (T == 128) {
     constexpr int C1 = BrSplitCfg<LOGN, S, 2>::CPB;
-    if (blocks(B, C1) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st);
+    if (blocks(B, C1) <= 3 * cus) return launch_br_split<LOGN, S, 2>(ek, ws, testvec, B, st, io);
     // as above: a partly filled last round runs as one-ciphertext blocks
     const int64_t round = int64_t{BrSplitCfg<LOGN, S, 8>::CPB} * cus;
     const int64_t tail = B % round;
-    if (tail == 0 || blocks(tail, C1) > 3 * cus) return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st);
+    if (tail == 0 || blocks(tail, C1) > 3 * cus) return launch_br_split<LOGN, S, 8>(ek, ws, testvec, B, st, io);
     const int64_t head = B - tail;
-    if (int rc = launch_br_split<LOGN, S, 8>(ek, ws, testvec, head, st)) return rc;
-    const Workspace rest{ws.abar + head * (ek->p.n + 1), ws.extract + head * (ek->p.N + 1)};
-    return launch_br_split<LOGN, S, 2>(ek, rest, testvec, tail, st);
+    if (int rc = launch_br_split<LOGN, S, 8>(ek, ws, testvec, head, st, io)) return rc;
+    return launch_br_split<LOGN, S, 2>(ek, ws_tail(ek, ws, io, head), testvec, tail, st, io_tail(ek, io, head));
   } else {
-    return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st);
+    return launch_br_blocks<LOGN, S, T / 64>(ek, ws, testvec, B, st, io);
   }
 }
 
@@ -1472,8 +1533,9 @@ int dispatch_ring(const tfhe_eval_key* ek, A... args) {
 
 template <int LOGN, int S>
 struct BrRun {
-  static int run(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* tv, int64_t B, hipStream_t st) {
-    return launch_br<LOGN, S>(ek, ws, tv, B, st);
+  static int run(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* tv, int64_t B, hipStream_t st,
+                 const BrIo& io) {
+    return launch_br<LOGN, S>(ek, ws, tv, B, st, io);
   }
 };
 template <int LOGN, int S>
@@ -1509,8 +1571,9 @@ int launch_prep(const tfhe_eval_key* ek, const PrepArgs& a, const Workspace& ws,
 }
 
 int launch_blind_rotate(const tfhe_eval_key* ek, const Workspace& ws, const uint32_t* testvec,
-                        int64_t B, void* stream) {
-  return dispatch_ring<BrRun>(ek, ws, testvec, B, static_cast<hipStream_t>(stream));
+                        int64_t B, void* stream, const BrIo* io) {
+  const BrIo none{};
+  return dispatch_ring<BrRun>(ek, ws, testvec, B, static_cast<hipStream_t>(stream), io ? *io : none);
 }
 
 int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B, int mode,
@@ -1554,6 +1617,12 @@ int launch_relu_sign(const tfhe_eval_key* ek, uint32_t* y, int32_t bits, int64_t
   hipLaunchKernelGGL(relu_sign_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
                      static_cast<hipStream_t>(stream), y, ek->p.n, bits, v_begin, count);
   return launch_status("relu_sign_kernel");
+}
+
+int launch_cmux_abar(const tfhe_eval_key* ek, const uint32_t* a, int64_t B, uint16_t* abar, void* stream) {
+  hipLaunchKernelGGL(cmux_abar_kernel, dim3(static_cast<unsigned>((B + 255) / 256)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), a, ek->p.N, B, abar);
+  return launch_status("cmux_abar_kernel");
 }
 
 int launch_not(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count, void* stream) {

@@ -78,6 +78,9 @@ _SIGNATURES = {
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
+    "tfhe_debug_mod_switch_batch": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _i64, _vp]),
+    "tfhe_debug_cmux_workspace_bytes": (_i64, [_vp, _i64]),
+    "tfhe_debug_cmux_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
     "tfhe_stage_timing": (ctypes.c_int, [ctypes.c_int]),
     "tfhe_stage_times": (ctypes.c_int, [_vp, _vp]),
 }
@@ -247,7 +250,10 @@ def tfhe_encrypt_torus(sk: SecretKey, seed: int, mu, first_index: int = 0) -> np
 
 def tfhe_decrypt_phase(sk: SecretKey, ct, key_kind: int = 0) -> np.ndarray:
     ct = _host_u32(ct)
-    dim = ct.shape[-1] - 1
+    dim = sk.params.n if key_kind == 0 else sk.params.N
+    if ct.ndim < 1 or ct.shape[-1] != dim + 1:
+        raise ValueError(f"rows of {ct.shape[-1] if ct.ndim else 0} words; key_kind {key_kind} decrypts "
+                         f"rows of {dim + 1}")
     count = ct.size // (dim + 1)
     out = np.zeros(count, np.uint32)
     _check(lib().tfhe_decrypt_phase(sk.handle, key_kind, _hptr(ct), count, _hptr(out)))
@@ -286,22 +292,35 @@ def tfhe_workspace_bytes(ek: EvalKey, batch: int) -> int:
     return int(v)
 
 
-def alloc_workspace(ek: EvalKey, batch: int):
+def _on(stream):
+    """Allocation context of buffers that a call on `stream` will use: torch's
+    caching allocator hands out blocks per stream, and a block last used on
+    another stream may still be in use there by queued work, so buffers for
+    a caller-given stream are allocated on that stream."""
+    import contextlib
+
     import torch
-    return torch.empty(max(tfhe_workspace_bytes(ek, batch), 256), dtype=torch.uint8,
-                       device=f"cuda:{ek.device}")
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
 
 
-def _empty(shape, ek: EvalKey):
+def alloc_workspace(ek: EvalKey, batch: int, stream=None):
     import torch
-    return torch.empty(shape, dtype=torch.int32, device=f"cuda:{ek.device}")
+    with _on(stream):
+        return torch.empty(max(tfhe_workspace_bytes(ek, batch), 256), dtype=torch.uint8,
+                           device=f"cuda:{ek.device}")
+
+
+def _empty(shape, ek: EvalKey, stream=None):
+    import torch
+    with _on(stream):
+        return torch.empty(shape, dtype=torch.int32, device=f"cuda:{ek.device}")
 
 
 def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=None, stream=None):
     B = ca.shape[0]
     n = ek.params.n
-    out = _empty((B, n + 1), ek) if out is None else out
-    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    out = _empty((B, n + 1), ek, stream) if out is None else out
+    ws = alloc_workspace(ek, B, stream) if workspace is None else workspace
     g = GATES[gate] if isinstance(gate, str) else int(gate)
     w = B * (n + 1)
     d = ek.device
@@ -312,8 +331,8 @@ def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=Non
 
 def tfhe_lut_bootstrap_batch(ek: EvalKey, x, testvec, out=None, workspace=None, stream=None):
     B = x.shape[0]
-    out = _empty((B, ek.params.n + 1), ek) if out is None else out
-    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    out = _empty((B, ek.params.n + 1), ek, stream) if out is None else out
+    ws = alloc_workspace(ek, B, stream) if workspace is None else workspace
     w, d = B * (ek.params.n + 1), ek.device
     _check(lib().tfhe_lut_bootstrap_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(testvec, ek.params.N, "testvec", d),
                                           _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, x, testvec, out, ws)))
@@ -322,8 +341,8 @@ def tfhe_lut_bootstrap_batch(ek: EvalKey, x, testvec, out=None, workspace=None, 
 
 def tfhe_bootstrap_extract_batch(ek: EvalKey, x, testvec=None, out=None, workspace=None, stream=None):
     B = x.shape[0]
-    out = _empty((B, ek.params.N + 1), ek) if out is None else out
-    ws = alloc_workspace(ek, B) if workspace is None else workspace
+    out = _empty((B, ek.params.N + 1), ek, stream) if out is None else out
+    ws = alloc_workspace(ek, B, stream) if workspace is None else workspace
     p, d = ek.params, ek.device
     tv = _dbuf(testvec, p.N, "testvec", d) if testvec is not None else ctypes.c_void_p(0)
     _check(lib().tfhe_bootstrap_extract_batch(ek.handle, _dbuf(x, B * (p.n + 1), "x", d), tv,
@@ -334,7 +353,7 @@ def tfhe_bootstrap_extract_batch(ek: EvalKey, x, testvec=None, out=None, workspa
 
 def tfhe_keyswitch_batch(ek: EvalKey, x, out=None, stream=None):
     B = x.shape[0]
-    out = _empty((B, ek.params.n + 1), ek) if out is None else out
+    out = _empty((B, ek.params.n + 1), ek, stream) if out is None else out
     p, d = ek.params, ek.device
     _check(lib().tfhe_keyswitch_batch(ek.handle, _dbuf(x, B * (p.N + 1), "x", d),
                                       _dbuf(out, B * (p.n + 1), "out", d), B, _stream(stream, d, x, out)))
@@ -345,10 +364,10 @@ def glyph_relu_batch(ek: EvalKey, x, bits: int, y=None, gate_begin: int = 0, gat
                      workspace=None, stream=None):
     V = x.shape[0]
     n = ek.params.n
-    y = _empty((V, bits, n + 1), ek) if y is None else y
+    y = _empty((V, bits, n + 1), ek, stream) if y is None else y
     if gate_end is None:
         gate_end = V * (bits - 1)
-    ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
+    ws = alloc_workspace(ek, gate_end - gate_begin, stream) if workspace is None else workspace
     w, d = V * bits * (n + 1), ek.device
     _check(lib().glyph_relu_batch(ek.handle, _dbuf(x, w, "x", d), _dbuf(y, w, "y", d), V, bits, gate_begin,
                                   gate_end, *_wsbuf(ws, d), _stream(stream, d, x, y, ws)))
@@ -361,10 +380,10 @@ def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate
     out [V][bits][n+1]; gates [gate_begin, gate_end) of the V*bits."""
     V, u_bits = u.shape[0], u.shape[1]
     bits = delta.shape[1]
-    out = _empty(tuple(delta.shape), ek) if out is None else out
+    out = _empty(tuple(delta.shape), ek, stream) if out is None else out
     if gate_end is None:
         gate_end = V * bits
-    ws = alloc_workspace(ek, gate_end - gate_begin) if workspace is None else workspace
+    ws = alloc_workspace(ek, gate_end - gate_begin, stream) if workspace is None else workspace
     row, d = ek.params.n + 1, ek.device
     _check(lib().glyph_irelu_batch(ek.handle, _dbuf(u, V * u_bits * row, "u", d), u_bits,
                                    _dbuf(delta, V * bits * row, "delta", d), _dbuf(out, V * bits * row, "out", d),
@@ -375,8 +394,8 @@ def glyph_irelu_batch(ek: EvalKey, u, delta, out=None, gate_begin: int = 0, gate
 def tfhe_mux_batch(ek: EvalKey, c, a, b, out=None, workspace=None, stream=None):
     """out[e] encrypts c[e] ? a[e] : b[e]; all [B][n+1] device."""
     B = c.shape[0]
-    out = _empty((B, ek.params.n + 1), ek) if out is None else out
-    ws = alloc_workspace(ek, 2 * B) if workspace is None else workspace
+    out = _empty((B, ek.params.n + 1), ek, stream) if out is None else out
+    ws = alloc_workspace(ek, 2 * B, stream) if workspace is None else workspace
     w, d = B * (ek.params.n + 1), ek.device
     _check(lib().tfhe_mux_batch(ek.handle, _dbuf(c, w, "c", d), _dbuf(a, w, "a", d), _dbuf(b, w, "b", d),
                                 _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, c, a, b, out, ws)))
@@ -390,10 +409,11 @@ def glyph_mux_lut_workspace_bytes(ek: EvalKey, V: int, msg_bits: int, out_bits: 
     return int(r)
 
 
-def alloc_mux_lut_workspace(ek: EvalKey, V: int, msg_bits: int, out_bits: int):
+def alloc_mux_lut_workspace(ek: EvalKey, V: int, msg_bits: int, out_bits: int, stream=None):
     import torch
-    return torch.empty(max(glyph_mux_lut_workspace_bytes(ek, V, msg_bits, out_bits), 1), dtype=torch.uint8,
-                       device=f"cuda:{ek.device}")
+    with _on(stream):
+        return torch.empty(max(glyph_mux_lut_workspace_bytes(ek, V, msg_bits, out_bits), 1), dtype=torch.uint8,
+                           device=f"cuda:{ek.device}")
 
 
 def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspace=None, stream=None):
@@ -404,8 +424,8 @@ def glyph_mux_lut_batch(ek: EvalKey, x, table, out_bits: int, out=None, workspac
     t = _host_u32(table)
     if t.size != 1 << msg_bits:
         raise ValueError(f"table needs {1 << msg_bits} entries")
-    out = _empty((V, out_bits, ek.params.n + 1), ek) if out is None else out
-    ws = alloc_mux_lut_workspace(ek, V, msg_bits, out_bits) if workspace is None else workspace
+    out = _empty((V, out_bits, ek.params.n + 1), ek, stream) if out is None else out
+    ws = alloc_mux_lut_workspace(ek, V, msg_bits, out_bits, stream) if workspace is None else workspace
     row, d = ek.params.n + 1, ek.device
     _check(lib().glyph_mux_lut_batch(ek.handle, _dbuf(x, V * msg_bits * row, "x", d), msg_bits, _hptr(t), out_bits,
                                      _dbuf(out, V * out_bits * row, "out", d), V, *_wsbuf(ws, d),
@@ -427,7 +447,7 @@ def tfhe_export_packing_key(sk: SecretKey) -> np.ndarray:
 def tfhe_pack_keyswitch_batch(ek: EvalKey, lwe, out=None, stream=None):
     """lwe [B][Z][n+1] -> TRLWE samples [B][2][N] (phase sum_z phase_z X^z)."""
     B, Z = lwe.shape[0], lwe.shape[1]
-    out = _empty((B, 2, ek.params.N), ek) if out is None else out
+    out = _empty((B, 2, ek.params.N), ek, stream) if out is None else out
     p, d = ek.params, ek.device
     _check(lib().tfhe_pack_keyswitch_batch(ek.handle, _dbuf(lwe, B * Z * (p.n + 1), "lwe", d), Z,
                                            _dbuf(out, B * 2 * p.N, "out", d), B, _stream(stream, d, lwe, out)))
@@ -438,7 +458,9 @@ def tfhe_sample_extract_batch(trlwe, K: int, out=None, stream=None):
     """TRLWE samples [B][2][N] -> LWE samples of coefficients 0..K-1, [B][K][N+1]."""
     import torch
     B, N = trlwe.shape[0], trlwe.shape[2]
-    out = torch.empty((B, K, N + 1), dtype=torch.int32, device=trlwe.device) if out is None else out
+    if out is None:
+        with _on(stream):
+            out = torch.empty((B, K, N + 1), dtype=torch.int32, device=trlwe.device)
     d = trlwe.device.index
     _check(lib().tfhe_sample_extract_batch(N, _dbuf(trlwe, B * 2 * N, "trlwe", d), B, K,
                                            _dbuf(out, B * K * (N + 1), "out", d), _stream(stream, d, trlwe, out)))
@@ -456,7 +478,9 @@ def tfhe_not_batch(x, out=None, stream=None):
     import torch
     dim = x.shape[-1] - 1
     count = x.numel() // (dim + 1)
-    out = torch.empty_like(x) if out is None else out
+    if out is None:
+        with _on(stream):
+            out = torch.empty_like(x)
     w = count * (dim + 1)
     _check(lib().tfhe_not_batch(dim, _dbuf(x, w, "x"), _dbuf(out, w, "out", x.device.index), count,
                                 _stream(stream, x.device.index, x, out)))
@@ -466,10 +490,59 @@ def tfhe_not_batch(x, out=None, stream=None):
 def tfhe_negacyclic_mul_batch(ek: EvalKey, d, b, out=None, stream=None):
     import torch
     B = d.shape[0]
-    out = torch.empty_like(b) if out is None else out
+    if out is None:
+        with _on(stream):
+            out = torch.empty_like(b)
     w, dev = B * ek.params.N, ek.device
     _check(lib().tfhe_negacyclic_mul_batch(ek.handle, _dbuf(d, w, "d", dev), _dbuf(b, w, "b", dev),
                                            _dbuf(out, w, "out", dev), B, _stream(stream, dev, d, b, out)))
+    return out
+
+
+# ------------------------------------------------------------ stage checks
+
+def tfhe_debug_mod_switch_batch(ek: EvalKey, x, gate=None, cb=None, out=None, stream=None):
+    """Modulus switch of x [B][n+1] (gate None), or of the pre-combination of
+    (x, cb) for a gate, to Z_2N: int16 tensor [B][n+1] holding the uint16 words."""
+    import torch
+    B, n, d = x.shape[0], ek.params.n, ek.device
+    g = -1 if gate is None else (GATES[gate] if isinstance(gate, str) else int(gate))
+    if g >= 0 and cb is None:
+        raise ValueError("a gate needs its second operand cb")
+    if out is None:
+        with _on(stream):
+            out = torch.empty((B, n + 1), dtype=torch.int16, device=f"cuda:{d}")
+    if out.element_size() != 2 or out.numel() < B * (n + 1):
+        raise ValueError("out: expected at least B * (n + 1) 16-bit words")
+    w = B * (n + 1)
+    pcb = _dbuf(cb, w, "cb", d) if g >= 0 else ctypes.c_void_p(0)
+    _check(lib().tfhe_debug_mod_switch_batch(ek.handle, g, _dbuf(x, w, "x", d), pcb, _dptr(out), B,
+                                             _stream(stream, d, x, cb, out)))
+    return out
+
+
+def tfhe_debug_cmux_batch(ek: EvalKey, bk_row, abar, acc_in, out=None, workspace=None, stream=None):
+    """One CMux step with a caller-given coefficient-domain key row bk_row
+    ([2l][2][N] host words) on the accumulators acc_in [B][2][N] with rotation
+    amounts abar [B] (device): returns acc_out [B][2][N]."""
+    import torch
+    p, d = ek.params, ek.device
+    B = acc_in.shape[0]
+    row = _host_u32(bk_row).ravel()
+    if row.size != 2 * p.l * 2 * p.N:
+        raise ValueError(f"bk_row: {row.size} words, a key row has {2 * p.l * 2 * p.N}")
+    with _on(stream):
+        if out is None:
+            out = torch.empty((B, 2, p.N), dtype=torch.int32, device=f"cuda:{d}")
+        if workspace is None:
+            nb = lib().tfhe_debug_cmux_workspace_bytes(ek.handle, B)
+            if nb < 0:
+                _check(int(nb))
+            workspace = torch.empty(max(int(nb), 256), dtype=torch.uint8, device=f"cuda:{d}")
+    w = B * 2 * p.N
+    _check(lib().tfhe_debug_cmux_batch(ek.handle, _hptr(row), _dbuf(abar, B, "abar", d), _dbuf(acc_in, w, "acc_in", d),
+                                       _dbuf(out, w, "out", d), B, *_wsbuf(workspace, d),
+                                       _stream(stream, d, abar, acc_in, out, workspace)))
     return out
 
 

@@ -60,11 +60,16 @@ def test_clock_is_read_from_the_marked_dpm_level():
     assert bench.ClockSampler(None).mhz() is None
 
 
-def test_clock_is_the_median_of_the_final_half_of_the_samples():
+def test_clock_is_the_median_of_the_timed_window():
     c = bench.ClockSampler(None)
-    c.samples = [1500, 1700, 2250, 2310, 2320, 2300]  # the driver's figure ramps up first
-    assert c.mhz(least=6) == 2310
-    assert c.mhz() is None  # too few samples for the figure to have settled
+    # the driver's figure ramps up while the GPU wakes (before the window),
+    # then reads the running clock
+    c.samples = [(0.0, 368), (0.1, 1500), (0.2, 1700), (1.0, 2310), (1.1, 2320), (1.2, 2300), (1.3, 2290),
+                 (1.4, 2330), (2.0, 500)]
+    assert c.window(1.0, 1.4) == [2310, 2320, 2300, 2290, 2330]
+    assert c.mhz(1.0, 1.4) == 2310
+    assert c.mhz(1.0, 1.3) is None  # fewer than 5 samples in the window
+    assert c.mhz(1.0, 1.3, least=4) == 2310
 
 
 @pytest.mark.gpu
@@ -89,4 +94,27 @@ def test_bench_line_has_every_field(config):
     roof = d["roofline"]
     assert roof["bound"] == "alu" and abs(roof["peak"] - 39.3216) < 1e-9
     assert 0 < roof["frac"] < 1 and abs(roof["frac"] - roof["achieved"] / roof["peak"]) < 1e-12
-    assert roof["clock_mhz"] is None  # too few samples in so short a run for the figure to settle
+    # the clock over the timed window (untimed steps let it settle first);
+    # a two-step window may hold too few samples for a figure
+    if roof["clock_samples"] >= 5:
+        assert 1000 < roof["clock_mhz"] <= 2500
+        assert abs(roof["frac_at_clock"] - roof["frac"] * 2400 / roof["clock_mhz"]) < 1e-9
+    hbm = d["hbm"]
+    assert hbm["peak_GBps"] == 8000 and hbm["algorithmic_GBps"] > 0
+    assert "gfx950" in d["device"]
+
+
+@pytest.mark.gpu
+def test_driver_length_run_reports_the_clock():
+    """A run of 20 timed steps after 5 warm-up steps (0.6 s of timed work)
+    reports the clock of its timed window and the roofline fraction at that
+    clock."""
+    import json
+    print("[bench-contract] bench.py --steps 20 --warmup 5", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "20", "--warmup", "5",
+                        "--no-cpu-baseline"], capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    roof = json.loads(r.stdout.strip().splitlines()[-1])["roofline"]
+    if roof["clock_samples"] == 0:
+        pytest.skip("the DPM table is not readable here")
+    assert roof["clock_mhz"] is not None and roof["frac_at_clock"] is not None

@@ -177,3 +177,18 @@ def test_counts_too_large_for_one_launch_are_refused():
     assert null_buffer(L.tfhe_not_batch(64, None, None, most, None))
     assert refused(L.tfhe_not_batch(64, None, None, most + 1, None))
     assert refused(L.tfhe_not_batch((1 << 31) - 1, None, None, 3, None))  # no overflow in dim + 1
+
+
+def test_decrypt_checks_the_row_width_of_its_key():
+    """tfhe_decrypt_phase strides by the dimension of the key it decrypts
+    with (n for key_kind 0, N for 1): rows of the other width are refused
+    before the C call, which would otherwise read past the buffer."""
+    sk = tfhe.tfhe_secret_keygen(TOY, 3)
+    ct = np.zeros((4, TOY["n"] + 1), np.uint32)
+    assert tfhe.tfhe_decrypt_phase(sk, ct, 0).shape == (4,)
+    with pytest.raises(ValueError, match="rows of"):
+        tfhe.tfhe_decrypt_phase(sk, ct, 1)
+    ext = np.zeros((2, 3, TOY["N"] + 1), np.uint32)
+    assert tfhe.tfhe_decrypt_phase(sk, ext, 1).shape == (2, 3)
+    with pytest.raises(ValueError, match="rows of"):
+        tfhe.tfhe_decrypt_phase(sk, ext, 0)
