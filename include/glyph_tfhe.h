@@ -318,6 +318,32 @@ int tfhe_not_batch(int32_t dim, const uint32_t* in, uint32_t* out, int64_t count
 int tfhe_negacyclic_mul_batch(const tfhe_eval_key* ek, const int32_t* d, const uint32_t* b,
                               uint32_t* c, int64_t B, void* stream);
 
+/* ------------------------------------------------ allocation-free call ---- */
+
+/* Bytes of the device array that tfhe_gate_bootstrap_batch_noalloc uses as
+ * its workspace: one copy per device, held from the library's first use on
+ * that device until the process ends. */
+#define TFHE_NOALLOC_SCRATCH_BYTES (64ll << 20)
+
+/* tfhe_gate_bootstrap_batch for callers that cannot allocate device memory
+ * -- code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation: the same kernels and results, with the workspace taken from a
+ * file-scope device array of TFHE_NOALLOC_SCRATCH_BYTES instead of from the
+ * caller.  The caller passes inputs and output as for
+ * tfhe_gate_bootstrap_batch (ca, cb, out: [B][n+1] device).  The call
+ * allocates nothing and records no stage-timing events; the first call on a
+ * device also looks up the array's address there.
+ * Limit: tfhe_workspace_bytes(ek, B) <= TFHE_NOALLOC_SCRATCH_BYTES (12,515
+ * gates at n = 630, N = 1024; 6,919 at n = 750, N = 2048); a larger batch
+ * returns TFHE_EINVAL, as do the argument errors of tfhe_gate_bootstrap_batch.
+ * Every call on a device shares that device's array: calls that can run at
+ * the same time on one device (on different streams, or unordered from
+ * different threads) race and corrupt each other's results.  Nothing in the
+ * array needs clearing between calls: every word is written before it is
+ * read. */
+int tfhe_gate_bootstrap_batch_noalloc(const tfhe_eval_key* ek, int gate, const uint32_t* ca,
+                                      const uint32_t* cb, uint32_t* out, int64_t B, void* stream);
+
 /* ------------------------------------------------------- stage checks ---- *
  * Single stages of the blind rotation, run by the production kernels in
  * their production launch shapes, so that a fault can be located in one step

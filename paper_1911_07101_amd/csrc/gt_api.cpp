@@ -147,7 +147,8 @@ struct StageScope {
   StageEvent ev{};
   bool on = false;
   hipStream_t st;
-  StageScope(int stage, void* stream) : st(static_cast<hipStream_t>(stream)) {
+  StageScope(int stage, void* stream, bool allowed = true) : st(static_cast<hipStream_t>(stream)) {
+    if (!allowed) return;
     std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof_on) return;
     ev.stage = stage;
@@ -454,20 +455,21 @@ int64_t tfhe_workspace_bytes(const tfhe_eval_key* ek, int64_t batch) {
   return workspace_bytes(ek->p, batch);
 }
 
+// timing: whether the stage-timing events (tfhe_stage_timing) may be recorded
 static int bootstrap_common(const tfhe_eval_key* ek, const PrepArgs& a, const uint32_t* testvec,
                             uint32_t* out, int out_mode, void* ws, int64_t ws_bytes, void* stream,
-                            bool keyswitch) {
+                            bool keyswitch, bool timing = true) {
   int rc = check_ws(ek, ws, ws_bytes, a.B);
   if (rc) return rc;
   DeviceGuard g(ek->device);
   if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
   Workspace w = carve_workspace(ek->p, ws, a.B);
   {
-    StageScope sc(0, stream);
+    StageScope sc(0, stream, timing);
     if ((rc = launch_prep(ek, a, w, stream))) return rc;
   }
   {
-    StageScope sc(1, stream);
+    StageScope sc(1, stream, timing);
     if ((rc = launch_blind_rotate(ek, w, testvec, a.B, stream))) return rc;
   }
   if (!keyswitch) {
@@ -475,13 +477,13 @@ static int bootstrap_common(const tfhe_eval_key* ek, const PrepArgs& a, const ui
                                   hipMemcpyDeviceToDevice, static_cast<hipStream_t>(stream));
     return e == hipSuccess ? TFHE_OK : hip_fail(e, "copy extracted samples");
   }
-  StageScope sc(2, stream);
+  StageScope sc(2, stream, timing);
   return launch_keyswitch(ek, w.extract, out, a.B, out_mode, a.bits, a.gate_begin, stream);
 }
 
-int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
-                              uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_,
-                              void* stream) {
+static int gate_bootstrap_impl(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
+                               uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_, void* stream,
+                               bool timing) {
   if (!ek) return fail(TFHE_EINVAL, "NULL eval key");
   if (B < 0) return fail(TFHE_EINVAL, "negative batch");
   if (int rc = check_count(B, ek->p.n + 1, "ciphertexts")) return rc;
@@ -494,7 +496,13 @@ int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t*
                            {{out, w, "out"}, {workspace, workspace_bytes(ek->p, B), "workspace"}})))
     return rc;
   PrepArgs a{kModeGate, gate, ca, cb, B, 0, 0};
-  return bootstrap_common(ek, a, nullptr, out, kModeGate, workspace, workspace_bytes_, stream, true);
+  return bootstrap_common(ek, a, nullptr, out, kModeGate, workspace, workspace_bytes_, stream, true, timing);
+}
+
+int tfhe_gate_bootstrap_batch(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb,
+                              uint32_t* out, int64_t B, void* workspace, int64_t workspace_bytes_,
+                              void* stream) {
+  return gate_bootstrap_impl(ek, gate, ca, cb, out, B, workspace, workspace_bytes_, stream, true);
 }
 
 int tfhe_lut_bootstrap_batch(const tfhe_eval_key* ek, const uint32_t* in, const uint32_t* testvec,
@@ -901,3 +909,8 @@ int tfhe_stage_times(double* ms, int64_t* launches) {
 }
 
 }  // extern "C"
+
+int gt::gate_bootstrap(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb, uint32_t* out,
+                       int64_t B, void* workspace, int64_t workspace_bytes, void* stream, bool timing) {
+  return gate_bootstrap_impl(ek, gate, ca, cb, out, B, workspace, workspace_bytes, stream, timing);
+}

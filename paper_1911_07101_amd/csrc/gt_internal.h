@@ -38,6 +38,10 @@ namespace gt {
 int fail(int rc, const char* fmt, ...);
 int check_params(const tfhe_params& p);
 
+// tfhe_gate_bootstrap_batch; timing = false records no stage-timing events
+int gate_bootstrap(const tfhe_eval_key* ek, int gate, const uint32_t* ca, const uint32_t* cb, uint32_t* out,
+                   int64_t B, void* workspace, int64_t workspace_bytes, void* stream, bool timing);
+
 // generator tags
 enum : uint32_t {
   kTagLweKey = 1, kTagRlweKey = 2, kTagBkMask = 3, kTagBkNoise = 4,

@@ -78,6 +78,7 @@ _SIGNATURES = {
     "tfhe_not_batch": (ctypes.c_int, [_i32, _vp, _vp, _i64, _vp]),
     "tfhe_negacyclic_mul_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_transform_error_bound": (ctypes.c_int, [_vp, _vp, _vp]),
+    "tfhe_gate_bootstrap_batch_noalloc": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_debug_mod_switch_batch": (ctypes.c_int, [_vp, ctypes.c_int, _vp, _vp, _vp, _i64, _vp]),
     "tfhe_debug_cmux_workspace_bytes": (_i64, [_vp, _i64]),
     "tfhe_debug_cmux_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
@@ -326,6 +327,21 @@ def tfhe_gate_bootstrap_batch(ek: EvalKey, gate, ca, cb, out=None, workspace=Non
     d = ek.device
     _check(lib().tfhe_gate_bootstrap_batch(ek.handle, g, _dbuf(ca, w, "ca", d), _dbuf(cb, w, "cb", d),
                                            _dbuf(out, w, "out", d), B, *_wsbuf(ws, d), _stream(stream, d, ca, cb, out, ws)))
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # TFHE_NOALLOC_SCRATCH_BYTES
+
+
+def tfhe_gate_bootstrap_batch_noalloc(ek: EvalKey, gate, ca, cb, out, stream=None):
+    """tfhe_gate_bootstrap_batch with the library's own device workspace (no
+    allocation anywhere in the call): out must be given; batches up to
+    tfhe_workspace_bytes(ek, B) <= NOALLOC_SCRATCH_BYTES."""
+    B = ca.shape[0]
+    w, d = B * (ek.params.n + 1), ek.device
+    g = GATES[gate] if isinstance(gate, str) else int(gate)
+    _check(lib().tfhe_gate_bootstrap_batch_noalloc(ek.handle, g, _dbuf(ca, w, "ca", d), _dbuf(cb, w, "cb", d),
+                                                   _dbuf(out, w, "out", d), B, _stream(stream, d, ca, cb, out)))
     return out
 
 
