@@ -261,24 +261,32 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   ek->bk_fft = nullptr;
   ek->tw = nullptr;
   ek->ksk = nullptr;
+  ek->ksk_mfma = nullptr;
   ek->pks = nullptr;
   ek->pks_bytes = 0;
   ek->key_tag = key_tag(*sk);
   // [n][2l][2 * parts][N/2] complex doubles
   ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
-  ek->ksk_bytes = static_cast<int64_t>(sk->ksk.size()) * 4;
+  // the key-switching key: as byte planes for the matrix-core key switching
+  // (t = 8, base 4), as is otherwise
+  const bool mfma_ks = ks_uses_mfma(p);
+  ek->ksk_bytes = mfma_ks ? 0 : static_cast<int64_t>(sk->ksk.size()) * 4;
+  ek->ksk_mfma_bytes = mfma_ks ? ksk_mfma_bytes(p) : 0;
   // forward tree twiddles, inverse stage twiddles, twist: N/2 complex each
   const int64_t tw_bytes = static_cast<int64_t>(3 * (p.N / 2)) * 16;
 
   std::vector<double> bk_host, tw(static_cast<size_t>(3 * p.N));
+  std::vector<int8_t> kmf_host;
   try {
     bk_host.resize(static_cast<size_t>(ek->bk_bytes / 8));
+    kmf_host.resize(static_cast<size_t>(ek->ksk_mfma_bytes));
   } catch (const std::bad_alloc&) {
     delete ek;
-    return fail(TFHE_ENOMEM, "host allocation failed for the transform-domain key");
+    return fail(TFHE_ENOMEM, "host allocation failed for the transformed keys");
   }
   bk_to_transform_host(p, ek->parts, sk->bk.data(), bk_host.data());
   twiddles_host(p.N, tw.data());
+  if (mfma_ks) ksk_to_mfma_host(p, sk->ksk.data(), kmf_host.data());
 
   int rc = TFHE_OK;
   hipError_t e;
@@ -289,10 +297,15 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   }
   if ((e = hipMalloc(&ek->bk_fft, ek->bk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(bk): %s", hipGetErrorString(e)); goto fail_out; }
   if ((e = hipMalloc(&ek->tw, tw_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(twiddles): %s", hipGetErrorString(e)); goto fail_out; }
-  if ((e = hipMalloc(&ek->ksk, ek->ksk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(ksk): %s", hipGetErrorString(e)); goto fail_out; }
   if ((e = hipMemcpy(ek->bk_fft, bk_host.data(), ek->bk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy bk"); goto fail_out; }
   if ((e = hipMemcpy(ek->tw, tw.data(), tw_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy twiddles"); goto fail_out; }
-  if ((e = hipMemcpy(ek->ksk, sk->ksk.data(), ek->ksk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy ksk"); goto fail_out; }
+  if (mfma_ks) {
+    if ((e = hipMalloc(&ek->ksk_mfma, ek->ksk_mfma_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(ksk): %s", hipGetErrorString(e)); goto fail_out; }
+    if ((e = hipMemcpy(ek->ksk_mfma, kmf_host.data(), ek->ksk_mfma_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy ksk"); goto fail_out; }
+  } else {
+    if ((e = hipMalloc(&ek->ksk, ek->ksk_bytes)) != hipSuccess) { rc = fail(TFHE_ENOMEM, "hipMalloc(ksk): %s", hipGetErrorString(e)); goto fail_out; }
+    if ((e = hipMemcpy(ek->ksk, sk->ksk.data(), ek->ksk_bytes, hipMemcpyHostToDevice)) != hipSuccess) { rc = hip_fail(e, "copy ksk"); goto fail_out; }
+  }
   *ek_out = ek;
   return TFHE_OK;
 
@@ -338,6 +351,7 @@ void tfhe_eval_key_free(tfhe_eval_key* ek) {
   if (ek->bk_fft) (void)hipFree(ek->bk_fft);
   if (ek->tw) (void)hipFree(ek->tw);
   if (ek->ksk) (void)hipFree(ek->ksk);
+  if (ek->ksk_mfma) (void)hipFree(ek->ksk_mfma);
   if (ek->pks) (void)hipFree(ek->pks);
   delete ek;
 }

@@ -389,6 +389,45 @@ void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, d
   parallel_for(static_cast<int64_t>(p.n) * 2 * p.l * 2, 16, bk_convert_rows, &ctx);
 }
 
+bool ks_uses_mfma(const tfhe_params& p) { return p.ks_t == 8 && p.ks_basebit == 2; }
+
+int64_t ksk_mfma_bytes(const tfhe_params& p) { return static_cast<int64_t>(p.N) * ksk_mfma_nb(p) * 4 * 64 * 16; }
+
+namespace {
+struct KmfCtx {
+  const tfhe_params* p;
+  const uint32_t* ksk;
+  int8_t* out;
+};
+
+void kmf_rows(int64_t begin, int64_t end, void* vctx) {
+  const KmfCtx& c = *static_cast<KmfCtx*>(vctx);
+  const int n = c.p->n;
+  const int64_t row = n + 1, nbs = ksk_mfma_nb(*c.p);
+  for (int64_t i = begin; i < end; i++)
+    for (int64_t nb = 0; nb < nbs; nb++)
+      for (int l = 0; l < 64; l++) {
+        const int64_t col = nb * 32 + l % 32;
+        for (int s = 0; s < 16; s++) {
+          const int j = 4 * (l / 32) + s / 4, v = s % 4;
+          int64_t x = 0;
+          if (v != 0 && col <= n) x = c.ksk[((i * 8 + j) * 3 + (v - 1)) * row + col];
+          // signed base-256 digits, the top one taken mod 256 (2^32 = 0)
+          for (int beta = 0; beta < 4; beta++) {
+            const int64_t b = ((x & 255) ^ 128) - 128;
+            x = (x - b) >> 8;
+            c.out[(((i * nbs + nb) * 4 + beta) * 64 + l) * 16 + s] = static_cast<int8_t>(b);
+          }
+        }
+      }
+}
+}  // namespace
+
+void ksk_to_mfma_host(const tfhe_params& p, const uint32_t* ksk, int8_t* out) {
+  KmfCtx ctx{&p, ksk, out};
+  parallel_for(p.N, 8, kmf_rows, &ctx);
+}
+
 void twiddles_host(int N, double* tw) {
   const int n = N / 2;
   const long double pi = 3.141592653589793238462643383279502884L;

@@ -23,7 +23,10 @@ struct tfhe_eval_key {
   int cus;          // compute units of the device (the blind rotation sizes its blocks by it)
   double* bk_fft;   // device [n][2l][2*parts][N/2] complex (re, im), transform layout, times 2/N
   double* tw;       // device [3][N/2] complex: forward tree twiddles, inverse stage twiddles, twist
-  uint32_t* ksk;    // device [N][t][base-1][n+1]
+  uint32_t* ksk;    // device [N][t][base-1][n+1], for key switching other than t = 8, base 4 (else NULL)
+  int8_t* ksk_mfma; // device, t = 8 and base 4: the key as signed byte planes in matrix-core operand
+                    // order (ksk_mfma_host), else NULL
+  int64_t ksk_mfma_bytes;
   uint32_t* pks;    // device packing key [n][t][base-1][2][N], or NULL until uploaded
   int64_t bk_bytes;
   int64_t ksk_bytes;
@@ -60,6 +63,21 @@ int key_part_bits(int parts);
 double transform_error_bound(const tfhe_params& p, int parts);
 int key_parts(const tfhe_params& p);  // 2 or 3, 0 if no split keeps the bound
 void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out);
+
+// Key switching with t = 8 digits of 2 bits runs on the matrix cores: the
+// key is uploaded as signed byte planes.  For input coefficient i, 32-column
+// block nb, byte plane beta and lane l of a 64-lane operand, 16 bytes at
+// (((i * NB + nb) * 4 + beta) * 64 + l) * 16, NB = ksk_mfma_nb(p); byte
+// s is byte plane beta of KSK[i][j][v - 1][col] with col = 32 nb + l % 32,
+// j = 4 (l / 32) + s / 4, v = s % 4 (0 when v = 0 or col > n).  The signed
+// bytes b_0..b_3 in [-128, 128) of a key word x satisfy
+// sum_beta b_beta 2^(8 beta) = x mod 2^32.
+// 32-column blocks of the layout, padded to whole pairs (a kernel block
+// covers two)
+inline int ksk_mfma_nb(const tfhe_params& p) { return (p.n + 1 + 63) / 64 * 2; }
+bool ks_uses_mfma(const tfhe_params& p);
+int64_t ksk_mfma_bytes(const tfhe_params& p);
+void ksk_to_mfma_host(const tfhe_params& p, const uint32_t* ksk, int8_t* out);
 void twiddles_host(int N, double* tw);
 void parallel_for(int64_t count, int64_t grain, void (*fn)(int64_t, int64_t, void*), void* ctx);
 

@@ -189,10 +189,17 @@ __device__ __forceinline__ void ct_butterfly(double2& xe, double2& xe2, double2 
 // k = n/2^(s+1) + j/2^(s+1) and multiplies by tw[k]).  In: pass-0 (coefficient)
 // layout; out: last-pass (transform) layout.  Each stage fetches its own
 // twiddles (one per butterfly group of the thread).
-template <class Lay, bool TW_PERMUTED, bool PRIO = false>
+struct NoHook {
+  __device__ void operator()() const {}
+};
+
+// hook() runs after the butterflies of pass HOOK_PASS (between that pass and
+// the next transpose)
+template <class Lay, bool TW_PERMUTED, bool PRIO = false, int HOOK_PASS = -1, class Hook = NoHook>
 __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2* scr,
                                             const double2* __restrict__ tw,
-                                            const double2* __restrict__ tw_uniform, int tree = 1) {
+                                            const double2* __restrict__ tw_uniform, int tree = 1,
+                                            Hook hook = {}) {
   constexpr int E = Lay::E;
   static_for<0, Lay::NPASS>([&](auto PI) {
     constexpr int p = decltype(PI)::value;
@@ -233,6 +240,7 @@ __device__ __forceinline__ void fft_forward(double2 (&x)[Lay::E], int t, double2
         });
       });
     });
+    if constexpr (p == HOOK_PASS) hook();
   });
 }
 
@@ -604,10 +612,20 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
 
   // One block barrier per CMux keeps the block's ciphertexts on the same
   // CMux: they then read the same key points close together in time, which
-  // the L1 cache serves.
+  // the L1 cache serves.  The block's second half of waves takes it later,
+  // after pass 1 of the third digit polynomial's forward transform (of the
+  // last, with fewer than three digits per polynomial), so that the two
+  // waves sharing a SIMD run about two digit transforms apart and one's
+  // transposes overlap the other's arithmetic (A/B on one machine: 28.34 ->
+  // 27.89 ms per 4096 bootstraps; offsets of one pass, one transform, one
+  // and a half transforms gave 0.2 % .. 1.1 %).
   constexpr bool kCmuxBarrier = CPB > 1 && T <= 64;
+  const bool late = kCmuxBarrier && slot >= CPB / 2;
+  const int late_digit = l > 2 ? 2 : l - 1;  // every wave takes exactly one barrier per CMux
   for (int i = 0; i < n; i++) {
-    if constexpr (kCmuxBarrier) __syncthreads();
+    if constexpr (kCmuxBarrier) {
+      if (!late) __syncthreads();
+    }
     const uint32_t a_i = ab[i];
     const __amdgpu_buffer_rsrc_t bkr =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(bk + static_cast<size_t>(i) * bk_step), 0,
@@ -651,7 +669,10 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
         for (int e = 0; e < E; e++)
           x[e] = make_double2(static_cast<double>(signed_field(D[0][e], dpos, dw)),
                               static_cast<double>(signed_field(D[1][e], dpos, dw)));
-        fft_forward<Lay, true>(x, t, scr, s_tw, tw_g);
+        const bool barrier_here = late && q == 0 && jj == late_digit;
+        fft_forward<Lay, true, false, 1>(x, t, scr, s_tw, tw_g, 1, [&] {
+          if (barrier_here) __syncthreads();
+        });
 #pragma unroll
         for (int o = 0; o < O; o++) {
           if (o > 0) {
@@ -838,25 +859,58 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
 
     for (int q = 0; q < 2; q++) {
       const uint32_t* P = q ? acc_b : acc_a;
-      // with two digits of at most 10 bits, the second digit of each of the
-      // lane's 4E coefficients is kept from the first digit's pass (three
-      // fields to a register) instead of being recomputed from LDS
+      // With two digits of at most 10 bits the second digit of each of the
+      // lane's 4E coefficients is kept packed (three fields to a register)
+      // from the first digit's pass.  For the mask polynomial (q = 0), right
+      // after the CMux's closing barrier, each wave forms D = X^{a_i} P - P
+      // (plus the decomposition offset) only at its own half's coefficients
+      // and writes the words to region h of its own and of its partner's
+      // transpose scratch (idle before the transforms): each scratch then
+      // holds both halves' words, region hh for half hh, and each wave reads
+      // them from its own; both digits are fields of one word, so one
+      // exchange serves both digit passes.  The body polynomial's digits are
+      // computed by each wave at both halves' coefficients from the
+      // accumulator: exchanging them too took one more barrier between the
+      // waves' transforms and was 2.7 % slower than this (A/B on one
+      // machine, 8192 lookups: 133.6 ms, against 135.9 ms exchanging
+      // neither polynomial and 137.3 ms exchanging both).  Other gadgets
+      // recompute D from the accumulator for every digit.
       uint32_t pk[(4 * E + 2) / 3];
-      for (int jj = 0; jj < l; jj++) {
-        const uint32_t dpos = static_cast<uint32_t>(32 - (jj + 1) * bg_bit), dw = static_cast<uint32_t>(bg_bit);
-        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
-        double2 w[E];
-#pragma unroll
-        for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>(e * 128 * 16));
-        // digit jj of D = X^{a_i} P - P (plus the decomposition offset),
-        // recomputed from LDS for each digit (holding D for both halves would
-        // take 4E registers): point j' + n/2 * hh of the subtree points
-        // j' = t + 64 e is coefficients j' + n/2 * hh (real part) and
-        // j' + n/2 * hh + n (imaginary part).  Then the splitting stage: this
-        // half's output u + w v (half 0) or u - w v (half 1).
+      const bool xq = packed_second && q == 0;
+      if (xq) {
         uint32_t a_q = a_i;
         int t_q = t;
         asm volatile("" : "+v"(a_q), "+v"(t_q));
+        __builtin_amdgcn_s_setprio(3);
+        uint4* mine = reinterpret_cast<uint4*>(scr) + 64 * (E / 2) * h + t;
+        uint4* theirs = reinterpret_cast<uint4*>(partner) + 64 * (E / 2) * h + t;
+#pragma unroll
+        for (int m = 0; m < E / 2; m++) {
+          uint32_t d[4];
+#pragma unroll
+          for (int k = 0; k < 4; k++) {  // (e, im) = (2m + k / 2, k % 2)
+            const int j = t_q + 64 * (2 * m + k / 2) + h * HN + (k % 2) * NC;
+            d[k] = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
+          }
+          const uint4 v = make_uint4(d[0], d[1], d[2], d[3]);
+          mine[64 * m] = v;
+          theirs[64 * m] = v;
+        }
+        __builtin_amdgcn_s_setprio(0);
+        __syncthreads();
+      }
+      for (int jj = 0; jj < l; jj++) {
+        const uint32_t dpos = static_cast<uint32_t>(32 - (jj + 1) * bg_bit), dw = static_cast<uint32_t>(bg_bit);
+        const uint32_t row = static_cast<uint32_t>((q * l + jj) * O * NC) * 16u;
+        // The splitting stage: this half's output u + w v (half 0) or
+        // u - w v (half 1) of point j' = t + 64 e, u and v the values of
+        // half 0 and half 1 there, i.e. coefficients j' + HN hh (real part)
+        // and j' + HN hh + NC (imaginary part), hh = 0, 1.
+        auto split = [&](const double (&dg)[2][2]) {
+          const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
+          return make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
+                              fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+        };
         double2 x[E];
         if (packed_second && jj == 1) {
           // the second digits, kept from the first digit's pass
@@ -870,16 +924,43 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
                 const int k = (e * 2 + hh) * 2 + im;
                 dg[hh][im] = static_cast<double>(signed_field(pk[k / 3], 10u * (k % 3), dw));
               }
-            const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
-            x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
-                                fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+            x[e] = split(dg);
+          }
+        } else if (xq) {
+          // the first digits from both halves' words; the second digits'
+          // fields packed for the next pass
+          const uint32_t dpos2 = dpos - dw;
+          const uint4* words = reinterpret_cast<const uint4*>(scr) + t;
+#pragma unroll
+          for (int m = 0; m < E / 2; m++) {
+            const uint4 w0 = words[64 * m], w1 = words[64 * (E / 2 + m)];
+            const uint32_t half_words[2][4] = {{w0.x, w0.y, w0.z, w0.w}, {w1.x, w1.y, w1.z, w1.w}};
+#pragma unroll
+            for (int ee = 0; ee < 2; ee++) {
+              const int e = 2 * m + ee;
+              double dg[2][2];
+#pragma unroll
+              for (int hh = 0; hh < 2; hh++)
+#pragma unroll
+                for (int im = 0; im < 2; im++) {
+                  const uint32_t D = half_words[hh][2 * ee + im];
+                  dg[hh][im] = static_cast<double>(signed_field(D, dpos, dw));
+                  const int k = (e * 2 + hh) * 2 + im;
+                  const uint32_t f = __builtin_amdgcn_ubfe(D, dpos2, dw);
+                  pk[k / 3] = k % 3 ? pk[k / 3] | (f << (10u * (k % 3))) : f;
+                }
+              x[e] = split(dg);
+            }
           }
         } else {
+          // digit jj of D at both halves' coefficients, from the accumulator
+          uint32_t a_q = a_i;
+          int t_q = t;
+          asm volatile("" : "+v"(a_q), "+v"(t_q));
           // raised issue priority while the digits' LDS reads are issued (as
-          // in the transposes): measured 7 % faster at N = 2048, where the
-          // two waves of a ciphertext wait on each other at the block barriers
+          // in the transposes), where the two waves of a ciphertext wait on
+          // each other at the block barriers
           __builtin_amdgcn_s_setprio(3);
-          const uint32_t dpos2 = dpos - dw;  // the second digit's field
 #pragma unroll
           for (int e = 0; e < E; e++) {
             double dg[2][2];
@@ -891,19 +972,20 @@ __global__ __launch_bounds__((BrSplitCfg<LOGN, S, WPB>::THREADS),
                 const uint32_t D = (rot_coef<NR>(P, a_q, j) - P[j] + offset) ^ flip;
                 dg[hh][im] = static_cast<double>(signed_field(D, dpos, dw));
                 if (packed_second) {
-                  // the second digit's field (its sign extension is the
-                  // digit, as for the first) packed three to a register
                   const int k = (e * 2 + hh) * 2 + im;
-                  const uint32_t f = __builtin_amdgcn_ubfe(D, dpos2, dw);
+                  const uint32_t f = __builtin_amdgcn_ubfe(D, dpos - dw, dw);
                   pk[k / 3] = k % 3 ? pk[k / 3] | (f << (10u * (k % 3))) : f;
                 }
               }
-            const double2 u = make_double2(dg[0][0], dg[0][1]), v = make_double2(dg[1][0], dg[1][1]);
-            x[e] = make_double2(fma(split_w.x, v.x, fma(-split_w.y, v.y, u.x)),
-                                fma(split_w.x, v.y, fma(split_w.y, v.x, u.y)));
+            x[e] = split(dg);
           }
           __builtin_amdgcn_s_setprio(0);
         }
+        // the key row's first output points, requested before the transform
+        // so that their latency overlaps it
+        double2 w[E];
+#pragma unroll
+        for (int e = 0; e < E; e++) w[e] = load_b128(bkr, voff, row + static_cast<uint32_t>(e * 128 * 16));
         fft_forward<Sub, true, true>(x, t, scr, tw_half, tw_g, 2 + h);
 #pragma unroll
         for (int o = 0; o < O; o++) {
@@ -1129,116 +1211,151 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
   }
 }
 
-// Key switching for t = 8 digits of 2 bits (16-bit precision), one sample per
-// thread.  A block of 256 threads covers 256 samples and COLS output
-// columns.  For each input coefficient i the block builds, in LDS, the pair
-// tables
-//   PT[p][u][col] = KSK[i][2p][u >> 2] + KSK[i][2p+1][u & 3]   (row of value 0 = 0)
-// for the 4 digit pairs p and the 16 pair values u; a thread then reads, for
-// each of its 4 pair values, the table row of that value with 16-byte loads
-// (4 columns each) and subtracts the 4 rows from its COLS outputs.  The
-// digits are taken once per sample and input coefficient, the row addresses
-// once per pair, and the column offsets are immediates.  Tables are
-// double-buffered across i (one barrier per i); the key rows are fetched
-// ahead.  Every table read, add and the final subtraction are exact
-// mod 2^32.
-constexpr int KS8_TAB = 64;                // 4 pairs x 16 pair values
+// Key switching for t = 8 digits of 2 bits on the matrix cores.  With
+// V[c][k] the indicator that digit j of sample c's rounded coefficient a_i
+// has value v (k = (i, j, v): 32 slots per input coefficient, 8 digits x 4
+// values, value 0 against a zero key row), key switching is the matrix
+// product
+//   out[c] = (0, b_c) - sum_k V[c][k] KSK[k]
+// with a 0/1 left factor.  The key is held as four signed byte planes
+// (ksk_to_mfma_host), so that each plane's product is an exact int8 x int8
+// product accumulated in int32 (at most 8 N non-zero terms of magnitude at
+// most 128 per output, far below 2^31), and the four products recombine
+// exactly mod 2^32.  One v_mfma_i32_32x32x32_i8 takes one input
+// coefficient's 32 slots: lane l holds the indicators of its sample
+// (32 samples per wave, sample l % 32) for digits 4 (l / 32) .. +3 as
+// one-hot bytes, and the key bytes of the same slots for column l % 32.
+// A block of KSM_WAVES waves covers 32 KSM_WAVES samples and 32 KSM_NB
+// columns over the input coefficients [i_begin, i_end); each coefficient's
+// key tile (KSM_NB column blocks x 4 planes x 64 lanes x 16 bytes) is
+// staged through LDS once per block (double-buffered, one barrier per
+// coefficient, fetched two coefficients ahead), and the inputs are fetched
+// KSM_CH coefficients at a time.  The coefficient range is split over
+// several blocks when that fills the GPU better: every block adds its exact
+// partial sum mod 2^32 to an output that keyswitch_init_kernel set to
+// (0, b), so the result does not depend on the order of the additions.
+constexpr int KSM_WAVES = 4;                      // waves per block, 32 samples each
+constexpr int KSM_NB = 2;                         // 32-column blocks per block (ksk_mfma_nb pads to it)
+constexpr int KSM_THREADS = 64 * KSM_WAVES;
+constexpr int KSM_SAMPLES = 32 * KSM_WAVES;       // samples per block
+constexpr int KSM_TILE = KSM_NB * 4 * 64;         // 16-byte units of one coefficient's key tile
+constexpr int KSM_UPT = KSM_TILE / KSM_THREADS;   // units each thread stages
+constexpr int KSM_CH = 8;                         // input coefficients fetched per load round
+static_assert(KSM_TILE % KSM_THREADS == 0, "whole units per thread");
 
-template <int COLS>
-__global__ __launch_bounds__(256) void keyswitch_t8b2_kernel(const uint32_t* __restrict__ in,
-                                                             const uint32_t* __restrict__ ksk,
-                                                             uint32_t* __restrict__ out, int n, int N,
-                                                             int64_t B, int mode, int32_t bits,
-                                                             int64_t gate_begin) {
-  constexpr int ROWS = 24;  // 8 digits x 3 non-zero values
-  constexpr int RS = COLS + 4;   // padded table row stride (words)
-  constexpr int VPT = COLS >= 16 ? 4 : COLS / 4;  // table entries each thread builds per (pair, half)
-  constexpr int PPT = COLS >= 16 ? COLS / 16 : 1;  // pairs each thread builds for
-  __shared__ __align__(16) uint32_t s_tab[2][KS8_TAB * RS];
-  const int tid = threadIdx.x;
-  const int64_t c = static_cast<int64_t>(blockIdx.x) * 256 + tid;
-  const bool c_ok = c < B;
-  const int col0 = blockIdx.y * COLS;
-  const size_t row = static_cast<size_t>(n) + 1;
-  const uint32_t* x_in = in + (c_ok ? c : B - 1) * (N + 1);
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
-  uint32_t acc[COLS];
-#pragma unroll
-  for (int j = 0; j < COLS; j++) acc[j] = col0 + j == n ? x_in[N] : 0u;
+struct KsmGrid {
+  int nb_total;      // 32-column blocks of the key layout
+  int col_tiles;     // nb_total / KSM_NB
+  int sample_tiles;  // ceil(B / KSM_SAMPLES)
+  int coef_len;      // input coefficients per block
+};
 
-  // table building: thread (p, col, half, g) = (tid / 4COLS % 4, tid % COLS,
-  // tid / COLS % 4, tid / 16COLS) fetches key rows of pair p at column
-  // col0 + col and writes the VPT entries u = 4 * half + v2, v2 in
-  // [g VPT, g VPT + VPT): PT[p][u] = row(2p, half) + row(2p+1, v2), row(., 0) = 0
-  const int b_col = tid % COLS, b_half = (tid / COLS) % 4, b_pair = (tid / (4 * COLS)) % 4;
-  const int b_v2 = COLS >= 16 ? 0 : (tid / (16 * COLS)) * VPT;
-  const bool b_ok = col0 + b_col <= n;
-  // key rows of coefficient i + d in kr[d] (element 0: row(2p, half),
-  // element 1 + v: row(2p+1, b_v2 + v)) and inputs x_i+d in xq[d]: both are
-  // fetched ahead (key rows three coefficients, inputs four), so their
-  // latency is covered by the table lookups in between
-  uint32_t kr[3][PPT][VPT + 1];
-  auto fetch = [&](int i, uint32_t (&kk)[PPT][VPT + 1]) {
-    const uint32_t* base = ksk + static_cast<size_t>(i) * ROWS * row + col0 + b_col;
+__global__ __launch_bounds__(KSM_THREADS, 2) void keyswitch_mfma_kernel(const uint32_t* __restrict__ in,
+                                                                     const i32x4* __restrict__ kmf,
+                                                                     uint32_t* __restrict__ out, int n, int N,
+                                                                     int64_t B, int mode, int32_t bits,
+                                                                     int64_t gate_begin, KsmGrid g) {
+  __shared__ i32x4 s_b[2][KSM_TILE];
+  const int st = static_cast<int>(blockIdx.x % g.sample_tiles);
+  const int ct = static_cast<int>((blockIdx.x / g.sample_tiles) % g.col_tiles);
+  const int kr = static_cast<int>(blockIdx.x / (static_cast<unsigned>(g.sample_tiles) * g.col_tiles));
+  const int i_begin = kr * g.coef_len;
+  const int i_end = min(N, i_begin + g.coef_len);
+  const int tid = threadIdx.x, w = tid / 64, l = tid % 64;
+  const int kg = l / 32;  // this lane's digits: 4 kg .. 4 kg + 3
+  const int64_t c = static_cast<int64_t>(st) * KSM_SAMPLES + 32 * w + (l % 32);
+  const uint32_t* x_in = in + (c < B ? c : B - 1) * (N + 1);
+  const int nb0 = ct * KSM_NB;
+
+  // key tile units: thread tid stages unit tid + KSM_THREADS u (column block
+  // nb0 + u, plane and lane tid / 64, tid % 64)
+  i32x4 breg[2][KSM_UPT];  // tiles of even and odd offset from i_begin
+  auto fetch = [&](int i, i32x4 (&dst)[KSM_UPT]) {
 #pragma unroll
-    for (int pp = 0; pp < PPT; pp++) {
-      const int pr = b_pair + pp * (4 / PPT);
-      uint32_t (&k)[VPT + 1] = kk[pp];
-      k[0] = (b_ok && b_half) ? base[static_cast<size_t>(pr * 6 + b_half - 1) * row] : 0u;
-#pragma unroll
-      for (int v = 0; v < VPT; v++) {
-        const int v2 = b_v2 + v;
-        k[1 + v] = (b_ok && v2) ? base[static_cast<size_t>(pr * 6 + 2 + v2) * row] : 0u;
-      }
-    }
+    for (int u = 0; u < KSM_UPT; u++)
+      dst[u] = kmf[(static_cast<int64_t>(i) * g.nb_total + nb0) * 256 + KSM_THREADS * u + tid];
   };
-  for (int d = 0; d < 3; d++) fetch(min(d, N - 1), kr[d]);
-  uint32_t xq[4];
+  fetch(i_begin, breg[0]);
+  fetch(min(i_begin + 1, N - 1), breg[1]);
+  // inputs: indices clamped to the row's last word N, inside the row
+  uint32_t xc[KSM_CH], xn[KSM_CH];
 #pragma unroll
-  for (int d = 0; d < 4; d++) xq[d] = x_in[min(d, N - 1)];
+  for (int k = 0; k < KSM_CH; k++) xc[k] = x_in[min(i_begin + k, N)];
+
+  i32x16 acc[KSM_NB][4];
+#pragma unroll
+  for (int nb = 0; nb < KSM_NB; nb++)
+#pragma unroll
+    for (int pl = 0; pl < 4; pl++)
+#pragma unroll
+      for (int r = 0; r < 16; r++) acc[nb][pl][r] = 0;
 
 #pragma unroll 1
-  for (int i = 0; i < N; i++) {
-    const int b = i & 1;
+  for (int i0 = i_begin; i0 < i_end; i0 += KSM_CH) {
+    if (i0 + KSM_CH < i_end) {
 #pragma unroll
-    for (int pp = 0; pp < PPT; pp++) {
-      uint32_t* tab = s_tab[b] + ((b_pair + pp * (4 / PPT)) * 16 + b_half * 4 + b_v2) * RS + b_col;
-#pragma unroll
-      for (int v = 0; v < VPT; v++) tab[v * RS] = kr[0][pp][0] + kr[0][pp][1 + v];
+      for (int k = 0; k < KSM_CH; k++) xn[k] = x_in[min(i0 + KSM_CH + k, N)];
     }
-    const uint32_t x = xq[0];
+    static_for<0, KSM_CH>([&](auto KI) {
+      constexpr int k = decltype(KI)::value;
+      const int i = i0 + k;
+      if (i >= i_end) return;  // uniform across the block
+      constexpr int b = k & 1;  // (i - i_begin) & 1: rounds start at even offsets
+      // stage this coefficient's tile (the buffer was last read two
+      // coefficients ago, before the previous barrier), fetch the tile two ahead
 #pragma unroll
-    for (int d = 0; d < 2; d++)
+      for (int u = 0; u < KSM_UPT; u++) s_b[b][KSM_THREADS * u + tid] = breg[b][u];
+      fetch(min(i + 2, N - 1), breg[b]);
+      __syncthreads();
+      // one-hot digit bytes of the sample: dword jj has byte d_j set, j = 4 kg + jj
+      const uint32_t r = (xc[k] + 0x8000u) >> 16;  // round to 16 bits, ties up
+      i32x4 a;
 #pragma unroll
-      for (int pp = 0; pp < PPT; pp++)
+      for (int jj = 0; jj < 4; jj++) a[jj] = static_cast<int32_t>(1u << (8u * ((r >> (14 - 2 * (4 * kg + jj))) & 3u)));
 #pragma unroll
-        for (int v = 0; v <= VPT; v++) kr[d][pp][v] = kr[d + 1][pp][v];
-    fetch(min(i + 3, N - 1), kr[2]);
+      for (int nb = 0; nb < KSM_NB; nb++)
 #pragma unroll
-    for (int d = 0; d < 3; d++) xq[d] = xq[d + 1];
-    xq[3] = x_in[min(i + 4, N - 1)];
-    __syncthreads();
-    const uint32_t r = (x + 0x8000u) >> 16;  // round to 16 bits, ties up
-    const uint32_t* tab = s_tab[b];
-    const uint4* rp[4];
+        for (int pl = 0; pl < 4; pl++)
+          acc[nb][pl] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, s_b[b][(nb * 4 + pl) * 64 + l], acc[nb][pl], 0, 0, 0);
+    });
 #pragma unroll
-    for (int p = 0; p < 4; p++)
-      rp[p] = reinterpret_cast<const uint4*>(tab + (p * 16 + ((r >> (12 - 4 * p)) & 15)) * RS);
-#pragma unroll
-    for (int q = 0; q < COLS / 4; q++) {
-      const uint4 s0 = rp[0][q], s1 = rp[1][q], s2 = rp[2][q], s3 = rp[3][q];
-      acc[4 * q + 0] -= (s0.x + s1.x) + (s2.x + s3.x);
-      acc[4 * q + 1] -= (s0.y + s1.y) + (s2.y + s3.y);
-      acc[4 * q + 2] -= (s0.z + s1.z) + (s2.z + s3.z);
-      acc[4 * q + 3] -= (s0.w + s1.w) + (s2.w + s3.w);
-    }
+    for (int k = 0; k < KSM_CH; k++) xc[k] = xn[k];
   }
 
-  if (!c_ok) return;
-  uint32_t* o = out + out_index(mode, c, bits, gate_begin) * row + col0;
+  // output register r of lane l: sample 8 (r / 4) + 4 (l / 32) + r % 4 of the
+  // wave, column l % 32 of the column block
+  const int row = n + 1;
+  static_for<0, 16>([&](auto RI) {
+    constexpr int r = decltype(RI)::value;
+    // one output row at a time (keeps the accumulators' copies out of VGPRs)
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t cs = static_cast<int64_t>(st) * KSM_SAMPLES + 32 * w + 8 * (r / 4) + 4 * kg + (r % 4);
+    if (cs >= B) return;
+    uint32_t* o = out + out_index(mode, cs, bits, gate_begin) * row;
 #pragma unroll
-  for (int j = 0; j < COLS; j++)
-    if (col0 + j <= n) o[j] = acc[j];
+    for (int nb = 0; nb < KSM_NB; nb++) {
+      const int col = (nb0 + nb) * 32 + (l % 32);
+      uint32_t sum = 0u;
+#pragma unroll
+      for (int pl = 0; pl < 4; pl++) sum += static_cast<uint32_t>(acc[nb][pl][r]) << (8 * pl);
+      if (col <= n) atomicAdd(o + col, 0u - sum);
+    }
+  });
+}
+
+// out = (0^n, b) for every sample: the starting value of the key switching
+// on the matrix cores, whose blocks add their partial sums to it
+__global__ __launch_bounds__(256) void keyswitch_init_kernel(const uint32_t* __restrict__ in, uint32_t* __restrict__ out,
+                                                             int n, int N, int64_t B, int mode, int32_t bits,
+                                                             int64_t gate_begin) {
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (idx >= B * (n + 1)) return;
+  const int64_t c = idx / (n + 1);
+  const int k = static_cast<int>(idx - c * (n + 1));
+  out[out_index(mode, c, bits, gate_begin) * (n + 1) + k] = k == n ? in[c * (N + 1) + N] : 0u;
 }
 
 __global__ __launch_bounds__(256) void relu_sign_kernel(uint32_t* __restrict__ y, int n, int32_t bits,
@@ -1584,22 +1701,31 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
                 p.ks_t * (1 << p.ks_basebit), KS_MAXROWS);
   dim3 grid(static_cast<unsigned>((B + KS_CB - 1) / KS_CB), static_cast<unsigned>((p.n + 1 + KS_COLS - 1) / KS_COLS));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (p.ks_t == 8 && p.ks_basebit == 2) {
-    // 32 output columns per block halve the table building and barriers per
-    // output, but only pay while the grid still gives every CU two blocks
-    // (4096 samples at n = 630: 16 columns, 0.87 ms against 1.02; 8192 at
-    // n = 750: 32 columns, 2.57 ms against 4.15)
+  if (ks_uses_mfma(p)) {
+    // split the input coefficients over k blocks per (sample tile, column
+    // tile) so that the rounds of resident blocks (two per CU) are full:
+    // the smallest ceil(tiles k / resident) ceil(N / k) for k <= 8
     const int64_t cus = ek->cus > 0 ? ek->cus : 256;
-    const int64_t sample_blocks = (B + 255) / 256;
-    if (sample_blocks * ((p.n + 1 + 31) / 32) >= 2 * cus) {
-      dim3 g8(static_cast<unsigned>(sample_blocks), static_cast<unsigned>((p.n + 1 + 31) / 32));
-      hipLaunchKernelGGL((keyswitch_t8b2_kernel<32>), g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
-                         bits, gate_begin);
-    } else {
-      dim3 g8(static_cast<unsigned>(sample_blocks), static_cast<unsigned>((p.n + 1 + 15) / 16));
-      hipLaunchKernelGGL((keyswitch_t8b2_kernel<16>), g8, dim3(256), 0, st, in, ek->ksk, out, p.n, p.N, B, mode,
-                         bits, gate_begin);
+    KsmGrid g;
+    g.nb_total = ksk_mfma_nb(p);
+    g.col_tiles = g.nb_total / KSM_NB;
+    const int64_t sample_tiles = (B + KSM_SAMPLES - 1) / KSM_SAMPLES;
+    g.sample_tiles = static_cast<int>(sample_tiles);
+    const int64_t tiles = sample_tiles * g.col_tiles, resident = 2 * cus;
+    int64_t best_k = 1, best = -1;
+    for (int64_t k = 1; k <= 8 && k <= p.N; k++) {
+      const int64_t len = (p.N + k - 1) / k, ranges = (p.N + len - 1) / len;
+      const int64_t cost = (tiles * ranges + resident - 1) / resident * len;
+      if (best < 0 || cost < best) best = cost, best_k = k;
     }
+    g.coef_len = static_cast<int>((p.N + best_k - 1) / best_k);
+    const int64_t ranges = (p.N + g.coef_len - 1) / g.coef_len;
+    const int64_t blocks = tiles * ranges;
+    hipLaunchKernelGGL(keyswitch_init_kernel, dim3(static_cast<unsigned>((B * (p.n + 1) + 255) / 256)), dim3(256), 0,
+                       st, in, out, p.n, p.N, B, mode, bits, gate_begin);
+    if (int rc = launch_status("keyswitch_init_kernel")) return rc;
+    hipLaunchKernelGGL(keyswitch_mfma_kernel, dim3(static_cast<unsigned>(blocks)), dim3(KSM_THREADS), 0, st, in,
+                       reinterpret_cast<const i32x4*>(ek->ksk_mfma), out, p.n, p.N, B, mode, bits, gate_begin, g);
   } else if (p.ks_t * (1 << p.ks_basebit) <= 32)
     hipLaunchKernelGGL((keyswitch_kernel<32>), grid, dim3(KS_COLS), 0, st, in, ek->ksk, out, p.n, p.N,
                        p.ks_t, p.ks_basebit, B, mode, bits, gate_begin);

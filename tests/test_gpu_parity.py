@@ -323,11 +323,11 @@ def test_keyswitch_parity_toy(torch):
 
 @pytest.mark.parametrize("B", [4096 + 3, 8192 + 5])
 def test_keyswitch_rounding_edges(torch, B):
-    """Key switching at n = 630, N = 1024 (t = 8, base 4) in both block widths
-    (16 output columns at 4096 samples, 32 at 8192), ragged: coefficients at
-    the rounding tie (half a step of 2^-16 rounds up), just below it, at 0,
-    all digits 3, and at the wrap (2^32 - 2^15 and above round to 0), bit for
-    bit against the oracle on spread rows."""
+    """Key switching at n = 630, N = 1024 (t = 8, base 4) on the matrix
+    cores, ragged in both the sample tiles and the split of the coefficient
+    range: coefficients at the rounding tie (half a step of 2^-16 rounds up),
+    just below it, at 0, all digits 3, and at the wrap (2^32 - 2^15 and above
+    round to 0), bit for bit against the oracle on spread rows."""
     p = wl.CONFIGS["tfhe128_nand"]["params"]
     N = p["N"]
     sk, ek, ok = keys_for("tfhe128_nand", torch)
@@ -341,6 +341,26 @@ def test_keyswitch_rounding_edges(torch, B):
     rows = np.unique(np.concatenate([np.arange(0, B, 7)[:96], np.linspace(0, B - 1, 64).astype(int)]))
     say(f"keyswitch edges B={B}, {len(rows)} rows checked")
     got = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, tfhe.to_device(x)))
+    assert np.array_equal(got[rows], oracle.keyswitch(ok, x[rows]))
+
+
+@pytest.mark.parametrize("B", [1, 127, 129, 1000, 8192 + 5])
+def test_keyswitch_parity_n750(torch, B):
+    """Key switching from N = 2048 to n = 750 (twelve 64-column tiles, the
+    last holding 47 columns): every batch size the launcher splits the 2048
+    coefficients differently for, from one sample (all coefficients spread
+    over many blocks) to 8197; all rows up to 1000 samples, spread rows
+    above."""
+    p = wl.CONFIGS["lut3_n2048"]["params"]
+    N = p["N"]
+    sk, ek, ok = keys_for("lut3_n2048", torch)
+    rng = np.random.default_rng(B)
+    x = rng.integers(0, M32, (B, N + 1), dtype=np.uint64).astype(np.uint32)
+    x[0, :N:5] = 0xFFFFFFFF  # all digits 3 and a wrap to 0
+    rows = np.arange(B) if B <= 1000 else np.unique(np.linspace(0, B - 1, 96).astype(int))
+    say(f"keyswitch n=750 B={B}, {len(rows)} rows checked")
+    got = tfhe.to_host(tfhe.tfhe_keyswitch_batch(ek, tfhe.to_device(x)))
+    assert got.shape == (B, p["n"] + 1)
     assert np.array_equal(got[rows], oracle.keyswitch(ok, x[rows]))
 
 
