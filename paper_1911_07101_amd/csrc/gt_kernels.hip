@@ -531,6 +531,14 @@ __global__ __launch_bounds__((BrCfg<LOGN, S, WPB>::THREADS), (BrCfg<LOGN, S, WPB
   using C = BrCfg<LOGN, S, WPB>;
   using Lay = typename C::Lay;
   constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
+  // Blocks of at most 4 waves are launched for batches that give every SIMD
+  // at most one wave.  Marking the accumulation registers used takes the
+  // wave's allocation past half the register file, so that the hardware
+  // places at most one wave per SIMD: without it a wave that fits in 256
+  // registers lets the dispatcher put up to six one-wave blocks on some CUs
+  // (their LDS allows it) and two waves on one SIMD, while other CUs idle
+  // (blind rotation of 1024 gates: 13.1 -> 10.0 ms, 3000 gates: 28.9 -> 25.9 ms)
+  if constexpr (C::MIN_WAVES == 1) asm volatile("" ::: "a255");
   __shared__ double2 s_tw[NC];
   __shared__ double2 s_scr[CPB * Lay::SCR];
   __shared__ uint32_t s_acc[CPB * 2 * NR];
