@@ -724,11 +724,14 @@ def test_tfhe128_nand_4096(torch):
 def test_block_shapes_for_small_batches(torch):
     """A batch that four one-wave blocks per CU hold (N = 1024: up to 1024
     gates) runs in blocks of one wave, a larger one in blocks of 8; at
-    N = 2048 up to three one-ciphertext blocks per CU (768 lookups), else
-    blocks of four ciphertexts.  Both sides of each boundary, with a ragged
-    last block, give the same samples as the full batch, and the last sample
-    of each size matches the oracle."""
-    for name, sizes in (("tfhe128_nand", (2100, 1025, 1024, 600, 7)), ("lut3_n2048", (1102, 769, 768, 100))):
+    N = 2048 up to two one-ciphertext blocks per CU (512 lookups) run one
+    wave per SIMD, up to three (768) with two, else blocks of four
+    ciphertexts, whose partly filled last round runs as one-ciphertext
+    blocks of either kind (1102 = 1024 + 78, 1600 = 1024 + 576).  Both sides
+    of each boundary, with a ragged last block, give the same samples as the
+    full batch, and the last sample of each size matches the oracle."""
+    for name, sizes in (("tfhe128_nand", (2100, 1025, 1024, 600, 7)),
+                        ("lut3_n2048", (1600, 1102, 769, 768, 513, 512, 100))):
         cfg = wl.CONFIGS[name]
         p = cfg["params"]
         sk, ek, ok = keys_for(name, torch)
