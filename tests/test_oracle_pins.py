@@ -280,6 +280,64 @@ def test_noiseless_cmux_selects():
             assert np.array_equal(poly_phase(out), oracle.rotate(poly_phase(acc), e % (2 * N)))
 
 
+def brute_cmux(N, l, bg, row, abar, acc):
+    """One CMux step written with the pure-Python pieces of brute_tfhe
+    (monomial, schoolbook product, carry-based decomposition)."""
+    X = brute.monomial(N, abar)
+    polys = [list(map(int, acc[0])), list(map(int, acc[1]))]
+    digit_polys = []
+    for P in polys:
+        D = [(x - y) % M32 for x, y in zip(brute.polymul_negacyclic(X, P), P)]
+        per = [brute.decompose(x, l, bg) for x in D]
+        digit_polys += [[per[m][j] for m in range(N)] for j in range(l)]
+    out = [list(P) for P in polys]
+    for r, dp in enumerate(digit_polys):
+        for q in range(2):
+            prod = brute.polymul_negacyclic(dp, list(map(int, row[r][q])))
+            out[q] = [(x + y) % M32 for x, y in zip(out[q], prod)]
+    return np.array(out, dtype=np.uint32)
+
+
+@pytest.mark.parametrize("l,bg", [(3, 7), (2, 10)])
+def test_cmux_with_a_given_key_row_matches_brute_force(l, bg):
+    """The oracle's CMux with a caller-given key row (the form the stage check
+    of one CMux uses) against the independent pure-Python CMux, with key rows
+    at the largest magnitudes of both signs and accumulators whose rotation
+    difference has every digit at -Bg/2 or Bg/2 - 1, and at random."""
+    N = 16
+    p = dict(TINY, l=l, bg_bit=bg)
+    rng = np.random.default_rng(l * 100 + bg)
+    half = 1 << (bg - 1)
+    rnd = 1 << (31 - l * bg) if l * bg < 32 else 0
+
+    def word_with_digits(d):
+        return (sum((d + half) << (32 - j * bg) for j in range(1, l + 1))
+                - sum(half << (32 - j * bg) for j in range(1, l + 1)) - rnd) % M32
+
+    rows = [np.full((2 * l, 2, N), w, np.uint32) for w in (0x80008000, 0x7FFF7FFF, 0xFFFFFFFF, 0x80000000)]
+    rows.append(rng.integers(0, M32, (2 * l, 2, N), dtype=np.uint64).astype(np.uint32))
+    accs = []
+    for d in (-half, half - 1):
+        w = word_with_digits(d)
+        assert brute.decompose(w, l, bg) == [d] * l
+        # X^N acc - acc = -2 acc: acc = -w / 2 gives the difference w (w even)
+        accs.append((np.full((2, N), (-(w // 2)) % M32, np.uint64).astype(np.uint32), N))
+    accs.append((rng.integers(0, M32, (2, N), dtype=np.uint64).astype(np.uint32), int(rng.integers(0, 2 * N))))
+    for row in rows:
+        for acc, abar in accs:
+            got = oracle.cmux_row(p, row, abar, acc)
+            assert np.array_equal(got, brute_cmux(N, l, bg, row, abar, acc))
+
+
+def test_mod_switch_array_matches_the_brute_force_rounding():
+    rng = np.random.default_rng(12)
+    for N in (16, 1024, 2048):
+        xs = np.concatenate([rng.integers(0, M32, 300, dtype=np.uint64),
+                             np.array([0, M32 - 1, M32 // (4 * N), M32 // (4 * N) - 1], dtype=np.uint64)]).astype(np.uint32)
+        got = oracle.mod_switch_array(xs.reshape(4, -1), N).ravel()
+        assert [int(g) for g in got] == [brute.mod_switch(int(x), N) for x in xs]
+
+
 # ---------------------------------------------------------------- semantics
 
 TRUTH = {"NAND": lambda a, b: 1 - (a & b), "AND": lambda a, b: a & b, "OR": lambda a, b: a | b,
