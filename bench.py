@@ -443,6 +443,49 @@ def suite(path: str):
         json.dump(recs, fh, indent=1)
 
 
+def issue_rate(iters: int):
+    """The VALU issue rate of each instruction kind the blind rotation uses
+    (tfhe_probe_valu_rate): 8 waves per SIMD, each running iters rounds of 16
+    instructions on 8 independent chains; lane-operations per CU per clock at
+    the clock read over the timed launches, against the 64 (4 SIMDs x 16
+    lanes) that the roofline's peak assumes.  One JSON line per kind."""
+    import torch
+
+    from paper_1911_07101_amd import tfhe
+
+    props = torch.cuda.get_device_properties(0)
+    cus = props.multi_processor_count
+    waves = cus * 4 * 8
+    out = torch.empty(waves * 64, dtype=torch.int32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    for kind in tfhe.PROBE_KINDS:
+        with ClockSampler(sclk_path()) as clock:
+            t_settle = time.perf_counter()
+            while time.perf_counter() - t_settle < 0.5:
+                tfhe.tfhe_probe_valu_rate(kind, waves, iters, out=out, stream=stream)
+                torch.cuda.synchronize()
+            times = []
+            t0 = time.perf_counter()
+            for _ in range(40):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                tfhe.tfhe_probe_valu_rate(kind, waves, iters, out=out, stream=stream)
+                e1.record(stream)
+                e1.synchronize()
+                times.append(e0.elapsed_time(e1))
+            t1 = time.perf_counter()
+        ms = sorted(times)[len(times) // 2]
+        lane_ops = waves * 64 * iters * 16
+        mhz = clock.mhz(t0, t1)
+        rate = lane_ops / (ms / 1e3)
+        print(json.dumps({
+            "probe": "valu_issue_rate", "instruction": kind, "waves": waves, "iters": iters,
+            "instructions_per_wave": iters * 16, "ms": ms, "lane_ops_per_s": rate,
+            "frac_of_peak_at_2400MHz": rate / PEAK_LANE_OPS, "clock_mhz": mhz,
+            "lane_ops_per_cu_per_clock": rate / cus / (mhz * 1e6) if mhz else None,
+            "device": f"{props.name} ({getattr(props, 'gcnArchName', '?')}, {cus} CUs)"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -457,6 +500,9 @@ def main():
                     help="before timing, run one plain device copy of this size (counter calibration)")
     ap.add_argument("--suite", metavar="PATH", default=None,
                     help="instead of the headline line, time every workload and write the records to PATH")
+    ap.add_argument("--issue-rate", type=int, metavar="ITERS", default=0,
+                    help="instead of the headline line, measure the VALU issue rate of each instruction kind "
+                         "the blind rotation uses (ITERS rounds of 8 instructions per wave)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the bootstrap batch has no cross-GPU step on this "
@@ -465,6 +511,9 @@ def main():
 
     if args.suite:
         suite(args.suite)
+        return
+    if args.issue_rate:
+        issue_rate(args.issue_rate)
         return
 
     import numpy as np

@@ -393,6 +393,18 @@ int tfhe_debug_cmux_batch(const tfhe_eval_key* ek, const uint32_t* bk_row, const
 int tfhe_stage_timing(int enable);
 int tfhe_stage_times(double* ms /*[3]*/, int64_t* launches /*[3]*/);
 
+/* VALU issue-rate probe, the measurement behind the blind rotation's
+ * roofline peak (64 lane-operations per CU per clock for full-rate
+ * instructions).  Launches waves / 4 blocks of 4 waves on `stream` (the
+ * current device); every wave runs iters rounds of 16 instructions of one
+ * kind on 8 independent chains -- 0: v_fma_f64, 1: v_add_u32,
+ * 2: v_cvt_f64_i32, 3: v_bfe_i32, 4: v_mul_lo_u32 -- and each lane
+ * writes one word to out[waves * 64] (device) so that no work is dropped.
+ * The caller times the launch.  Errors: TFHE_EINVAL for kind outside 0..4,
+ * waves not a positive multiple of 4 up to 2^20, iters outside [1, 2^24],
+ * or out NULL; TFHE_EHIP if the launch fails. */
+int tfhe_probe_valu_rate(int kind, int64_t waves, int64_t iters, uint32_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

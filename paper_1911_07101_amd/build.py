@@ -15,7 +15,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libglyph_tfhe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["gt_kernels.hip", "gt_api.cpp", "gt_host.cpp", "gt_noalloc.hip"]
+SOURCES = ["gt_kernels.hip", "gt_api.cpp", "gt_host.cpp", "gt_noalloc.hip", "gt_probe.hip"]
 COMMON = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-Wall", "-Wextra",
           "-Wno-unused-parameter", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
           # packed fp32 instructions stay off: ordinary float code only

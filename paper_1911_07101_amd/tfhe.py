@@ -84,6 +84,7 @@ _SIGNATURES = {
     "tfhe_debug_cmux_batch": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _i64, _vp, _i64, _vp]),
     "tfhe_stage_timing": (ctypes.c_int, [ctypes.c_int]),
     "tfhe_stage_times": (ctypes.c_int, [_vp, _vp]),
+    "tfhe_probe_valu_rate": (ctypes.c_int, [ctypes.c_int, _i64, _i64, _vp, _vp]),
 }
 
 
@@ -577,3 +578,21 @@ def tfhe_stage_times() -> dict:
     n = (ctypes.c_int64 * 3)()
     _check(lib().tfhe_stage_times(ms, n))
     return {STAGES[k]: (ms[k], n[k]) for k in range(3)}
+
+
+PROBE_KINDS = ("v_fma_f64", "v_add_u32", "v_cvt_f64_i32", "v_bfe_i32", "v_mul_lo_u32")
+
+
+def tfhe_probe_valu_rate(kind, waves: int, iters: int, out=None, stream=None):
+    """Launch the VALU issue-rate probe for one instruction kind (a name of
+    PROBE_KINDS or its index) on the current device; returns the [waves * 64]
+    output tensor.  The caller times the launch on `stream`."""
+    import torch
+    k = PROBE_KINDS.index(kind) if isinstance(kind, str) else int(kind)
+    dev = torch.cuda.current_device()
+    if out is None:
+        with _on(stream):
+            out = torch.empty(waves * 64, dtype=torch.int32, device=f"cuda:{dev}")
+    _check(lib().tfhe_probe_valu_rate(k, waves, iters, _dbuf(out, waves * 64, "out", dev), _stream(stream, dev, out)))
+    return out
+

@@ -118,3 +118,24 @@ def test_driver_length_run_reports_the_clock():
     if roof["clock_samples"] == 0:
         pytest.skip("the DPM table is not readable here")
     assert roof["clock_mhz"] is not None and roof["frac_at_clock"] is not None
+
+
+@pytest.mark.gpu
+def test_issue_rate_probe_lines():
+    """bench.py --issue-rate prints one line per instruction kind; the fp64
+    FMA runs at no more than the issue model's 64 lane-operations per CU per
+    clock and the 32-bit kinds at no more than twice that (CDNA4's 32-bit
+    VALU rate), within the clock reading's error."""
+    import json
+    print("[bench-contract] bench.py --issue-rate 2000", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--issue-rate", "2000"],
+                       capture_output=True, text=True, timeout=240)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [json.loads(x) for x in r.stdout.strip().splitlines()]
+    rate = {d["instruction"]: d for d in lines}
+    assert sorted(rate) == sorted(("v_fma_f64", "v_add_u32", "v_cvt_f64_i32", "v_bfe_i32", "v_mul_lo_u32"))
+    for d in lines:
+        assert d["ms"] > 0 and d["lane_ops_per_s"] > 0
+        limit = 64 if d["instruction"] in ("v_fma_f64", "v_cvt_f64_i32") else 128
+        if d["lane_ops_per_cu_per_clock"] is not None:
+            assert d["lane_ops_per_cu_per_clock"] <= limit * 1.05, d

@@ -192,3 +192,22 @@ def test_decrypt_checks_the_row_width_of_its_key():
     assert tfhe.tfhe_decrypt_phase(sk, ext, 1).shape == (2, 3)
     with pytest.raises(ValueError, match="rows of"):
         tfhe.tfhe_decrypt_phase(sk, ext, 0)
+
+
+def test_issue_rate_probe_refuses_bad_arguments():
+    """tfhe_probe_valu_rate checks its arguments before any HIP call (the
+    output pointer is NULL or the arguments are out of range, so nothing
+    here can reach a launch)."""
+    L = tfhe.lib()
+
+    def einval(rc, what):
+        return rc == tfhe.TFHE_EINVAL and what in L.tfhe_last_error().decode()
+
+    assert einval(L.tfhe_probe_valu_rate(5, 4, 1, None, None), "kind")
+    assert einval(L.tfhe_probe_valu_rate(-1, 4, 1, None, None), "kind")
+    assert einval(L.tfhe_probe_valu_rate(0, 6, 1, None, None), "waves")
+    assert einval(L.tfhe_probe_valu_rate(0, 0, 1, None, None), "waves")
+    assert einval(L.tfhe_probe_valu_rate(0, (1 << 20) + 4, 1, None, None), "waves")
+    assert einval(L.tfhe_probe_valu_rate(0, 4, 0, None, None), "iters")
+    assert einval(L.tfhe_probe_valu_rate(0, 4, (1 << 24) + 1, None, None), "iters")
+    assert einval(L.tfhe_probe_valu_rate(0, 4, 1, None, None), "NULL")
