@@ -874,7 +874,14 @@ int tfhe_debug_cmux_batch(const tfhe_eval_key* ek, const uint32_t* bk_row, const
   uint16_t* ab = reinterpret_cast<uint16_t*>(base + debug_cmux_key_bytes(ek));
   hipError_t e = hipMemcpyAsync(base, row.data(), row.size() * 8, hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return hip_fail(e, "copy key row");
-  if ((rc = launch_cmux_abar(ek, abar, B, ab, stream))) return rc;
+  // the host copy of the key row must outlive the upload: every return from
+  // here on waits for the stream first
+  auto finish = [&](int result) {
+    const hipError_t se = hipStreamSynchronize(st);
+    if (result != TFHE_OK) return result;
+    return se == hipSuccess ? TFHE_OK : hip_fail(se, "stage check");
+  };
+  if ((rc = launch_cmux_abar(ek, abar, B, ab, stream))) return finish(rc);
   BrIo io;
   io.acc_in = acc_in;
   io.acc_out = acc_out;
@@ -882,11 +889,9 @@ int tfhe_debug_cmux_batch(const tfhe_eval_key* ek, const uint32_t* bk_row, const
   io.n = 1;
   {
     StageScope sc(1, stream);
-    if ((rc = launch_blind_rotate(ek, Workspace{ab, nullptr}, nullptr, B, stream, &io))) return rc;
+    if ((rc = launch_blind_rotate(ek, Workspace{ab, nullptr}, nullptr, B, stream, &io))) return finish(rc);
   }
-  // the host copy of the key row must outlive the upload
-  e = hipStreamSynchronize(st);
-  return e == hipSuccess ? TFHE_OK : hip_fail(e, "stage check");
+  return finish(TFHE_OK);
 }
 
 int tfhe_stage_timing(int enable) {
