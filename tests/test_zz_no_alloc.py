@@ -72,3 +72,57 @@ def test_noalloc_gate_bootstrap_matches_the_workspace_entry(torch, cfg_name):
                                              most + 1, None)
     assert rc == tfhe.TFHE_EINVAL and "workspace" in L.tfhe_last_error().decode()
     say(f"{cfg_name}: a batch of {most + 1} refused, {most} fit")
+
+
+def test_noalloc_gate_bootstrap_in_a_captured_graph(torch):
+    """The entry point's purpose: a call recorded into a HIP graph (torch's
+    graph capture on a side stream; the call allocates nothing and records
+    no memory set) and replayed three times, with eager work and new inputs
+    copied into the captured buffers between the replays, gives each time
+    word for word what the workspace entry point gives on the same inputs
+    (128-bit parameters, 3000 NAND gates: 8-wave blocks and a one-wave
+    tail)."""
+    cfg = wl.CONFIGS["tfhe128_nand"]
+    p = cfg["params"]
+    say("keygen tfhe128_nand (graph)")
+    sk, ek = tfhe.tfhe_keygen_from_seed(p, cfg["key_seed"], 0)
+    L = tfhe.lib()
+    B = 3000
+    rng = np.random.default_rng(73)
+
+    def inputs(seed):
+        a, b = rng.integers(0, 2, B), rng.integers(0, 2, B)
+        ca = tfhe.tfhe_encrypt_torus(sk, seed, tfhe.encode_bits(a), 0)
+        cb = tfhe.tfhe_encrypt_torus(sk, seed, tfhe.encode_bits(b), B)
+        return a, b, ca, cb
+
+    a, b, ca_h, cb_h = inputs(80)
+    ca, cb = tfhe.to_device(ca_h), tfhe.to_device(cb_h)
+    out = torch.zeros((B, p["n"] + 1), dtype=torch.int32, device="cuda:0")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    nand = tfhe.GATES["NAND"]
+    with torch.cuda.stream(side):  # eager call first: the array's address is looked up outside the capture
+        assert L.tfhe_gate_bootstrap_batch_noalloc(ek.handle, nand, tfhe._dptr(ca), tfhe._dptr(cb), tfhe._dptr(out),
+                                                   B, ctypes.c_void_p(side.cuda_stream)) == tfhe.TFHE_OK
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    say("capture")
+    with torch.cuda.graph(graph, stream=side):
+        rc = L.tfhe_gate_bootstrap_batch_noalloc(ek.handle, nand, tfhe._dptr(ca), tfhe._dptr(cb), tfhe._dptr(out),
+                                                 B, ctypes.c_void_p(side.cuda_stream))
+    assert rc == tfhe.TFHE_OK, L.tfhe_last_error()
+    for replay in range(3):
+        if replay:
+            a, b, ca_h, cb_h = inputs(80 + replay)
+            ca.copy_(tfhe.to_device(ca_h))
+            cb.copy_(tfhe.to_device(cb_h))
+        out.fill_(0)  # eager work between the replays
+        torch.cuda.synchronize()
+        say(f"replay {replay}")
+        graph.replay()
+        torch.cuda.synchronize()
+        ref = tfhe.to_host(tfhe.tfhe_gate_bootstrap_batch(ek, "NAND", ca, cb))
+        got = tfhe.to_host(out)
+        assert np.array_equal(got, ref), f"replay {replay}: {int((got != ref).any(axis=1).sum())} of {B} gates differ"
+        assert np.array_equal(_bits(tfhe.tfhe_decrypt_phase(sk, got)), 1 - (a & b))
