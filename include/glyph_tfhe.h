@@ -204,7 +204,11 @@ int tfhe_bootstrap_extract_batch(const tfhe_eval_key* ek, const uint32_t* in,
 /* LWE key switching (Section 3.2) from dimension N under S to dimension n
  * under s: each a_i is rounded to ks_t*ks_basebit bits, split into ks_t
  * digits (most significant first) and the key entries of the non-zero digits
- * are subtracted from (0, b).  in: [B][N+1], out: [B][n+1], device. */
+ * are subtracted from (0, b).  in: [B][N+1], out: [B][n+1], device.  With
+ * t = 8 digits of base 4 the sum runs on the matrix cores (an exact int8
+ * product of the one-hot digits with the key's byte planes, whose partial
+ * sums over coefficient ranges are added to out with device-scope atomics:
+ * the result does not depend on their order). */
 int tfhe_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out, int64_t B,
                          void* stream);
 
