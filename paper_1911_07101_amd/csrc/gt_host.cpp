@@ -391,7 +391,7 @@ void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, d
 
 bool ks_uses_mfma(const tfhe_params& p) { return p.ks_t == 8 && p.ks_basebit == 2; }
 
-int64_t ksk_mfma_bytes(const tfhe_params& p) { return static_cast<int64_t>(p.N) * ksk_mfma_nb(p) * 4 * 64 * 16; }
+int64_t ksk_mfma_bytes(const tfhe_params& p) { return static_cast<int64_t>(p.N) / 4 * 3 * ksk_mfma_nb(p) * 4 * 64 * 16; }
 
 namespace {
 struct KmfCtx {
@@ -400,32 +400,40 @@ struct KmfCtx {
   int8_t* out;
 };
 
+// groups [begin, end) of four input coefficients
 void kmf_rows(int64_t begin, int64_t end, void* vctx) {
   const KmfCtx& c = *static_cast<KmfCtx*>(vctx);
   const int n = c.p->n;
   const int64_t row = n + 1, nbs = ksk_mfma_nb(*c.p);
-  for (int64_t i = begin; i < end; i++)
-    for (int64_t nb = 0; nb < nbs; nb++)
-      for (int l = 0; l < 64; l++) {
-        const int64_t col = nb * 32 + l % 32;
-        for (int s = 0; s < 16; s++) {
-          const int j = 4 * (l / 32) + s / 4, v = s % 4;
-          int64_t x = 0;
-          if (v != 0 && col <= n) x = c.ksk[((i * 8 + j) * 3 + (v - 1)) * row + col];
-          // signed base-256 digits, the top one taken mod 256 (2^32 = 0)
-          for (int beta = 0; beta < 4; beta++) {
-            const int64_t b = ((x & 255) ^ 128) - 128;
-            x = (x - b) >> 8;
-            c.out[(((i * nbs + nb) * 4 + beta) * 64 + l) * 16 + s] = static_cast<int8_t>(b);
+  for (int64_t grp = begin; grp < end; grp++)
+    for (int m = 0; m < 3; m++) {
+      const int64_t t = 3 * grp + m;
+      for (int64_t nb = 0; nb < nbs; nb++)
+        for (int l = 0; l < 64; l++) {
+          const int64_t col = nb * 32 + l % 32;
+          const int h = l / 32;
+          for (int s = 0; s < 16; s++) {
+            const int q = m < 2 ? h + 2 * m : h + 2 * (s / 8);
+            const int v = m < 2 ? 1 + s / 8 : 3;
+            const int w = m < 2 ? (s / 4) % 2 : (s % 8) / 4;
+            const int j = 7 - s % 4 - 4 * w;
+            const int64_t i = 4 * grp + q;
+            int64_t x = col <= n ? c.ksk[((i * 8 + j) * 3 + (v - 1)) * row + col] : 0;
+            // signed base-256 digits, the top one taken mod 256 (2^32 = 0)
+            for (int beta = 0; beta < 4; beta++) {
+              const int64_t b = ((x & 255) ^ 128) - 128;
+              x = (x - b) >> 8;
+              c.out[(((t * nbs + nb) * 4 + beta) * 64 + l) * 16 + s] = static_cast<int8_t>(b);
+            }
           }
         }
-      }
+    }
 }
 }  // namespace
 
 void ksk_to_mfma_host(const tfhe_params& p, const uint32_t* ksk, int8_t* out) {
   KmfCtx ctx{&p, ksk, out};
-  parallel_for(p.N, 8, kmf_rows, &ctx);
+  parallel_for(p.N / 4, 2, kmf_rows, &ctx);
 }
 
 void twiddles_host(int N, double* tw) {

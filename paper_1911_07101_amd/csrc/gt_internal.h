@@ -65,13 +65,17 @@ int key_parts(const tfhe_params& p);  // 2 or 3, 0 if no split keeps the bound
 void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out);
 
 // Key switching with t = 8 digits of 2 bits runs on the matrix cores: the
-// key is uploaded as signed byte planes.  For input coefficient i, 32-column
+// key is uploaded as signed byte planes, without the rows of digit value 0
+// (which select nothing).  The 96 key rows (j, v = 1..3) of four input
+// coefficients 4G + q make three tiles t = 3G + m.  For tile t, 32-column
 // block nb, byte plane beta and lane l of a 64-lane operand, 16 bytes at
-// (((i * NB + nb) * 4 + beta) * 64 + l) * 16, NB = ksk_mfma_nb(p); byte
-// s is byte plane beta of KSK[i][j][v - 1][col] with col = 32 nb + l % 32,
-// j = 4 (l / 32) + s / 4, v = s % 4 (0 when v = 0 or col > n).  The signed
-// bytes b_0..b_3 in [-128, 128) of a key word x satisfy
-// sum_beta b_beta 2^(8 beta) = x mod 2^32.
+// (((t * NB + nb) * 4 + beta) * 64 + l) * 16, NB = ksk_mfma_nb(p); byte s
+// is byte plane beta of KSK[4G + q][j][v - 1][col] with col = 32 nb + l % 32
+// (0 when col > n), h = l / 32 and
+//   m = 0, 1: q = h + 2 m, v = 1 + s / 8, w = (s / 4) % 2,
+//   m = 2:    q = h + 2 (s / 8), v = 3, w = (s % 8) / 4,
+// j = 7 - s % 4 - 4 w.  The signed bytes b_0..b_3 in [-128, 128) of a key
+// word x satisfy sum_beta b_beta 2^(8 beta) = x mod 2^32.
 // 32-column blocks of the layout, padded to whole pairs (a kernel block
 // covers two)
 inline int ksk_mfma_nb(const tfhe_params& p) { return (p.n + 1 + 63) / 64 * 2; }

@@ -1233,35 +1233,46 @@ __global__ __launch_bounds__(64) void keyswitch_kernel(const uint32_t* __restric
 
 // Key switching for t = 8 digits of 2 bits on the matrix cores.  With
 // V[c][k] the indicator that digit j of sample c's rounded coefficient a_i
-// has value v (k = (i, j, v): 32 slots per input coefficient, 8 digits x 4
-// values, value 0 against a zero key row), key switching is the matrix
-// product
+// has value v, for the 24 slots k = (i, j, v) of each input coefficient
+// (8 digits x the values 1..3: value 0 selects no key row), key switching
+// is the matrix product
 //   out[c] = (0, b_c) - sum_k V[c][k] KSK[k]
 // with a 0/1 left factor.  The key is held as four signed byte planes
 // (ksk_to_mfma_host), so that each plane's product is an exact int8 x int8
 // product accumulated in int32 (at most 8 N non-zero terms of magnitude at
 // most 128 per output, far below 2^31), and the four products recombine
-// exactly mod 2^32.  One v_mfma_i32_32x32x32_i8 takes one input
-// coefficient's 32 slots: lane l holds the indicators of its sample
-// (32 samples per wave, sample l % 32) for digits 4 (l / 32) .. +3 as
-// one-hot bytes, and the key bytes of the same slots for column l % 32.
-// A block of KSM_WAVES waves covers 32 KSM_WAVES samples and 32 KSM_NB
-// columns over the input coefficients [i_begin, i_end); each coefficient's
-// key tile (KSM_NB column blocks x 4 planes x 64 lanes x 16 bytes) is
-// staged through LDS once per block (double-buffered, one barrier per
-// coefficient, fetched two coefficients ahead), and the inputs are fetched
+// exactly mod 2^32.  The 96 slots of four consecutive coefficients
+// 4G + q make three v_mfma_i32_32x32x32_i8 (key tiles T = 3G + m): lane l
+// of a wave (sample l % 32 of 32, column l % 32 of a 32-column block) holds
+// 16 slots, those of coefficient q = h (m = 0) or h + 2 (m = 1) for values
+// 1 and 2, and those of value 3 of both (m = 2), h = l / 32.  The
+// indicator bytes come from the digits spread one per byte (digits 7..4 of
+// the rounded coefficient in the bytes of the low word, 3..0 in the high)
+// and one byte permutation per word and value.
+// A block of KSM_WAVES waves covers KSM_SAMPLES samples and 32 KSM_NB
+// columns over the input coefficients [i_begin, i_end); a wave covers 64 of
+// the samples (two MFMA row groups sharing each key fragment) and one
+// column block.  Each key tile (KSM_NB column blocks x 4 planes x 64 lanes
+// x 16 bytes) is staged through LDS once per block (double-buffered, one
+// barrier per tile, the fragments read one tile ahead of their products and
+// the tile fetched five ahead), and the inputs are staged through LDS
 // KSM_CH coefficients at a time.  The coefficient range is split over
 // several blocks when that fills the GPU better: every block adds its exact
 // partial sum mod 2^32 to an output that keyswitch_init_kernel set to
 // (0, b), so the result does not depend on the order of the additions.
-constexpr int KSM_WAVES = 4;                      // waves per block, 32 samples each
+constexpr int KSM_WAVES = 4;                      // waves per block
 constexpr int KSM_NB = 2;                         // 32-column blocks per block (ksk_mfma_nb pads to it)
 constexpr int KSM_THREADS = 64 * KSM_WAVES;
-constexpr int KSM_SAMPLES = 32 * KSM_WAVES;       // samples per block
-constexpr int KSM_TILE = KSM_NB * 4 * 64;         // 16-byte units of one coefficient's key tile
+constexpr int KSM_SG = 2;                         // 32-sample groups per wave
+constexpr int KSM_SAMPLES = 128;                  // samples per block
+constexpr int KSM_TILE = KSM_NB * 4 * 64;         // 16-byte units of one key tile
 constexpr int KSM_UPT = KSM_TILE / KSM_THREADS;   // units each thread stages
-constexpr int KSM_CH = 8;                         // input coefficients fetched per load round
+constexpr int KSM_CH = 8;                         // input coefficients staged per round
+constexpr int KSM_STEPS = KSM_CH / 4 * 3;         // key tiles per round
+constexpr int KSM_RING = 3;                       // key tiles in flight in registers
+static_assert(KSM_WAVES == KSM_NB * KSM_SAMPLES / (32 * KSM_SG), "waves tile the block's samples x columns");
 static_assert(KSM_TILE % KSM_THREADS == 0, "whole units per thread");
+static_assert(KSM_STEPS % KSM_RING == 0 && KSM_STEPS % 2 == 0, "ring and LDS buffer indices repeat every round");
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
@@ -1270,8 +1281,20 @@ struct KsmGrid {
   int nb_total;      // 32-column blocks of the key layout
   int col_tiles;     // nb_total / KSM_NB
   int sample_tiles;  // ceil(B / KSM_SAMPLES)
-  int coef_len;      // input coefficients per block
+  int coef_len;      // input coefficients per block, a multiple of KSM_CH
 };
+
+// the 2-bit fields of the byte b, one per byte: field f of b in byte f
+__device__ __forceinline__ uint32_t spread_digits(uint32_t b) {
+  return (b | (b << 6) | (b << 12) | (b << 18)) & 0x03030303u;
+}
+
+// byte f of the result is 1 where byte f of the spread digits d equals v
+// (v_perm_b32 picks byte d_f of the table, whose byte v is 1)
+template <int V>
+__device__ __forceinline__ int32_t digit_indicator(uint32_t d) {
+  return static_cast<int32_t>(__builtin_amdgcn_perm(0u, 1u << (8 * V), d));
+}
 
 __global__ __launch_bounds__(KSM_THREADS, 2) void keyswitch_mfma_kernel(const uint32_t* __restrict__ in,
                                                                      const i32x4* __restrict__ kmf,
@@ -1279,6 +1302,7 @@ __global__ __launch_bounds__(KSM_THREADS, 2) void keyswitch_mfma_kernel(const ui
                                                                      int64_t B, int mode, int32_t bits,
                                                                      int64_t gate_begin, KsmGrid g) {
   __shared__ i32x4 s_b[2][KSM_TILE];
+  __shared__ i32x4 s_x[2][KSM_SAMPLES * 3];  // [buffer][sample][12 words, 8 used]
   // Workgroups are handed to the 8 XCDs in turn (workgroup b to XCD b mod 8),
   // and each XCD has its own L2.  The logical tile index L runs over the
   // workgroups of one XCD before the next (a bijection on [0, G) for any G),
@@ -1293,83 +1317,149 @@ __global__ __launch_bounds__(KSM_THREADS, 2) void keyswitch_mfma_kernel(const ui
   const int i_begin = kr * g.coef_len;
   const int i_end = min(N, i_begin + g.coef_len);
   const int tid = threadIdx.x, w = tid / 64, l = tid % 64;
-  const int kg = l / 32;  // this lane's digits: 4 kg .. 4 kg + 3
-  const int64_t c = static_cast<int64_t>(st) * KSM_SAMPLES + 32 * w + (l % 32);
-  const uint32_t* x_in = in + (c < B ? c : B - 1) * (N + 1);
+  const bool hi = l >= 32;  // this lane's coefficients of each four: 1 and 3 (else 0 and 2)
+  // wave w: samples [64 (w % 2), +64) of the block's tile as two groups of
+  // 32, column block w / 2 of the tile's KSM_NB
+  const int ws = w % 2, wc = w / 2;
+  // inputs: thread tid loads words 4 (tid % 2) .. +3 of the round's KSM_CH
+  // from row tid / 2 of the block's samples
+  static_assert(KSM_CH == 8 && KSM_THREADS == 2 * KSM_SAMPLES, "one 16-byte load per thread per round");
+  const int xs = tid / 2, xh = tid % 2;
+  const uint32_t* x_row;
+  {
+    const int64_t c = static_cast<int64_t>(st) * KSM_SAMPLES + xs;
+    x_row = in + (c < B ? c : B - 1) * (N + 1) + 4 * xh;
+  }
   const int nb0 = ct * KSM_NB;
 
   // key tile units: thread tid stages unit tid + KSM_THREADS u (column block
   // nb0 + u, plane and lane tid / 64, tid % 64)
-  i32x4 breg[2][KSM_UPT];  // tiles of even and odd offset from i_begin
-  auto fetch = [&](int i, i32x4 (&dst)[KSM_UPT]) {
+  const int t_begin = i_begin / 4 * 3, t_last = N / 4 * 3 - 1;
+  i32x4 breg[KSM_RING][KSM_UPT];
+  auto fetch = [&](int t, i32x4 (&dst)[KSM_UPT]) {
 #pragma unroll
     for (int u = 0; u < KSM_UPT; u++)
-      dst[u] = kmf[(static_cast<int64_t>(i) * g.nb_total + nb0) * 256 + KSM_THREADS * u + tid];
+      dst[u] = kmf[(static_cast<int64_t>(min(t, t_last)) * g.nb_total + nb0) * 256 + KSM_THREADS * u + tid];
   };
-  fetch(i_begin, breg[0]);
-  fetch(min(i_begin + 1, N - 1), breg[1]);
-  // inputs: indices clamped to the row's last word N, inside the row
-  uint32_t xc[KSM_CH], xn[KSM_CH];
+  // the first two tiles go to LDS now; breg[s % KSM_RING] holds the tile of
+  // offset s + 2 from t_begin at step s
 #pragma unroll
-  for (int k = 0; k < KSM_CH; k++) xc[k] = x_in[min(i_begin + k, N)];
+  for (int d = 0; d < 2; d++) {
+    fetch(t_begin + d, breg[d]);
+#pragma unroll
+    for (int u = 0; u < KSM_UPT; u++) s_b[d][KSM_THREADS * u + tid] = breg[d][u];
+  }
+#pragma unroll
+  for (int d = 0; d < KSM_RING; d++) fetch(t_begin + 2 + d, breg[d]);
+  // (coef_len and N are multiples of KSM_CH, so a round ends before word N)
+  i32x4 xv;
+  __builtin_memcpy(&xv, x_row + i_begin, 16);
+  s_x[0][3 * xs + xh] = xv;
+  uint32_t xc[KSM_SG][KSM_CH];
+  uint32_t sp[KSM_SG][4];  // spread digits: low and high word of this lane's two coefficients
+  int xb = 0;
+  // this wave's key fragments (4 planes of its column block): fr[s & 1] holds
+  // tile s's, read from LDS one step before its products
+  i32x4 fr[2][4];
+  __syncthreads();
+#pragma unroll
+  for (int pl = 0; pl < 4; pl++) fr[0][pl] = s_b[0][(wc * 4 + pl) * 64 + l];
 
-  i32x16 acc[KSM_NB][4];
+  i32x16 acc[KSM_SG][4];
 #pragma unroll
-  for (int nb = 0; nb < KSM_NB; nb++)
+  for (int gi = 0; gi < KSM_SG; gi++)
 #pragma unroll
     for (int pl = 0; pl < 4; pl++)
 #pragma unroll
-      for (int r = 0; r < 16; r++) acc[nb][pl][r] = 0;
+      for (int r = 0; r < 16; r++) acc[gi][pl][r] = 0;
 
 #pragma unroll 1
   for (int i0 = i_begin; i0 < i_end; i0 += KSM_CH) {
-    if (i0 + KSM_CH < i_end) {
-#pragma unroll
-      for (int k = 0; k < KSM_CH; k++) xn[k] = x_in[min(i0 + KSM_CH + k, N)];
-    }
-    static_for<0, KSM_CH>([&](auto KI) {
-      constexpr int k = decltype(KI)::value;
-      const int i = i0 + k;
-      if (i >= i_end) return;  // uniform across the block
-      constexpr int b = k & 1;  // (i - i_begin) & 1: rounds start at even offsets
-      // stage this coefficient's tile (the buffer was last read two
-      // coefficients ago, before the previous barrier), fetch the tile two ahead
-#pragma unroll
-      for (int u = 0; u < KSM_UPT; u++) s_b[b][KSM_THREADS * u + tid] = breg[b][u];
-      fetch(min(i + 2, N - 1), breg[b]);
+    const bool more = i0 + KSM_CH < i_end;
+    const int t0 = i0 / 4 * 3;
+    if (more) __builtin_memcpy(&xv, x_row + i0 + KSM_CH, 16);
+    static_for<0, KSM_STEPS>([&](auto SI) {
+      constexpr int s = decltype(SI)::value;
+      constexpr int b = s & 1;  // (t - t_begin) & 1: rounds start at even offsets
+      constexpr int grp = s / 3, m = s % 3;
+      const int t = t0 + s;
+      // Step of tile t: after the barrier, read the fragments of tile t + 1
+      // (it went to LDS one step ago), then stage tile t + 2 in the buffer
+      // that held t's (read one step ago, before this barrier) and fetch
+      // tile t + 5; the products of t use the fragments read one step ago.
+      if constexpr (s == KSM_STEPS - 1)
+        if (more) s_x[xb ^ 1][3 * xs + xh] = xv;
       __syncthreads();
-      // one-hot digit bytes of the sample: dword jj has byte d_j set, j = 4 kg + jj
-      const uint32_t r = (xc[k] + 0x8000u) >> 16;  // round to 16 bits, ties up
-      i32x4 a;
 #pragma unroll
-      for (int jj = 0; jj < 4; jj++) a[jj] = static_cast<int32_t>(1u << (8u * ((r >> (14 - 2 * (4 * kg + jj))) & 3u)));
+      for (int pl = 0; pl < 4; pl++) fr[b ^ 1][pl] = s_b[b ^ 1][(wc * 4 + pl) * 64 + l];
 #pragma unroll
-      for (int nb = 0; nb < KSM_NB; nb++)
+      for (int u = 0; u < KSM_UPT; u++) s_b[b][KSM_THREADS * u + tid] = breg[s % KSM_RING][u];
+      fetch(t + 2 + KSM_RING, breg[s % KSM_RING]);
+      if constexpr (s == 0) {
 #pragma unroll
-        for (int pl = 0; pl < 4; pl++)
-          acc[nb][pl] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a, s_b[b][(nb * 4 + pl) * 64 + l], acc[nb][pl], 0, 0, 0);
+        for (int gi = 0; gi < KSM_SG; gi++) {
+          const int sl = 32 * (KSM_SG * ws + gi) + (l % 32);
+#pragma unroll
+          for (int q = 0; q < 2; q++) {
+            const i32x4 v = s_x[xb][3 * sl + q];
+#pragma unroll
+            for (int e = 0; e < 4; e++) xc[gi][4 * q + e] = static_cast<uint32_t>(v[e]);
+          }
+        }
+      }
+      if constexpr (m == 0) {
+        // this lane's coefficients 4 grp + (0 or 1) and 4 grp + (2 or 3),
+        // rounded to 16 bits (ties up), their digits spread one per byte
+#pragma unroll
+        for (int gi = 0; gi < KSM_SG; gi++)
+#pragma unroll
+          for (int q = 0; q < 2; q++) {
+            const uint32_t x = hi ? xc[gi][4 * grp + 2 * q + 1] : xc[gi][4 * grp + 2 * q];
+            const uint32_t r = (x + 0x8000u) >> 16;
+            sp[gi][2 * q] = spread_digits(r & 0xffu);
+            sp[gi][2 * q + 1] = spread_digits(r >> 8);
+          }
+      }
+      i32x4 a[KSM_SG];
+#pragma unroll
+      for (int gi = 0; gi < KSM_SG; gi++) {
+        if constexpr (m < 2) {
+          a[gi][0] = digit_indicator<1>(sp[gi][2 * m]);
+          a[gi][1] = digit_indicator<1>(sp[gi][2 * m + 1]);
+          a[gi][2] = digit_indicator<2>(sp[gi][2 * m]);
+          a[gi][3] = digit_indicator<2>(sp[gi][2 * m + 1]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; e++) a[gi][e] = digit_indicator<3>(sp[gi][e]);
+        }
+      }
+#pragma unroll
+      for (int pl = 0; pl < 4; pl++)
+#pragma unroll
+        for (int gi = 0; gi < KSM_SG; gi++)
+          acc[gi][pl] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[gi], fr[b][pl], acc[gi][pl], 0, 0, 0);
     });
-#pragma unroll
-    for (int k = 0; k < KSM_CH; k++) xc[k] = xn[k];
+    xb ^= 1;
   }
 
-  // output register r of lane l: sample 8 (r / 4) + 4 (l / 32) + r % 4 of the
-  // wave, column l % 32 of the column block
+  // output register r of lane l: sample 8 (r / 4) + 4 (l / 32) + r % 4 of
+  // the group, column l % 32 of the wave's column block
   const int row = n + 1;
+  const int col = (nb0 + wc) * 32 + (l % 32);
+  if (col > n) return;
   static_for<0, 16>([&](auto RI) {
     constexpr int r = decltype(RI)::value;
     // one output row at a time (keeps the accumulators' copies out of VGPRs)
     __builtin_amdgcn_sched_barrier(0);
-    const int64_t cs = static_cast<int64_t>(st) * KSM_SAMPLES + 32 * w + 8 * (r / 4) + 4 * kg + (r % 4);
-    if (cs >= B) return;
-    uint32_t* o = out + out_index(mode, cs, bits, gate_begin) * row;
 #pragma unroll
-    for (int nb = 0; nb < KSM_NB; nb++) {
-      const int col = (nb0 + nb) * 32 + (l % 32);
+    for (int gi = 0; gi < KSM_SG; gi++) {
+      const int64_t cs = static_cast<int64_t>(st) * KSM_SAMPLES + 32 * (KSM_SG * ws + gi) + 8 * (r / 4) +
+                         4 * (l / 32) + (r % 4);
+      if (cs >= B) continue;
       uint32_t sum = 0u;
 #pragma unroll
-      for (int pl = 0; pl < 4; pl++) sum += static_cast<uint32_t>(acc[nb][pl][r]) << (8 * pl);
-      if (col <= n) atomicAdd(o + col, 0u - sum);
+      for (int pl = 0; pl < 4; pl++) sum += static_cast<uint32_t>(acc[gi][pl][r]) << (8 * pl);
+      atomicAdd(out + out_index(mode, cs, bits, gate_begin) * row + col, 0u - sum);
     }
   });
 }
@@ -1752,7 +1842,7 @@ int launch_keyswitch(const tfhe_eval_key* ek, const uint32_t* in, uint32_t* out,
       const int64_t cost = (tiles * ranges + resident - 1) / resident * len;
       if (best < 0 || cost < best) best = cost, best_k = k;
     }
-    g.coef_len = static_cast<int>((p.N + best_k - 1) / best_k);
+    g.coef_len = static_cast<int>(((p.N + best_k - 1) / best_k + KSM_CH - 1) / KSM_CH * KSM_CH);
     const int64_t ranges = (p.N + g.coef_len - 1) / g.coef_len;
     const int64_t blocks = tiles * ranges;
     hipLaunchKernelGGL(keyswitch_init_kernel, dim3(static_cast<unsigned>((B * (p.n + 1) + 255) / 256)), dim3(256), 0,
