@@ -8,9 +8,12 @@
 //                          SampleExtract; one wave per ciphertext (N <= 1024)
 //   blind_rotate_split_kernel  the same with two waves per ciphertext, each
 //                          computing one half of every transform (N = 2048)
-//   keyswitch_t8b2_kernel  LWE key switching back to dimension n (t = 8, base 4)
+//   keyswitch_init_kernel, keyswitch_mfma_kernel  LWE key switching back to
+//                          dimension n for t = 8, base 4: (0, b), then an exact
+//                          int8 product on the matrix cores added to it
 //   keyswitch_kernel       the same for any other digit count and base
 //   relu_sign_kernel       trivial 0 for the sign bit of the ReLU output
+//   cmux_abar_kernel       modulus-switched inputs of a one-CMux stage check
 //   not_kernel             NOT without bootstrapping
 //   pack_init_kernel, pack_ks_kernel  functional key switching of LWE samples
 //                          into one ring sample
