@@ -279,9 +279,12 @@ int64_t glyph_mux_lut_workspace_bytes(const tfhe_eval_key* ek, int64_t V, int32_
  * v in [1, 2^ks_basebit), is a TRLWE sample under S of the constant
  * polynomial v * s_i * 2^(32 - (j+1)*ks_basebit), noise alpha_bk) and add it
  * to the eval key on its device.  n * ks_t * (2^ks_basebit - 1) * 2N words
- * (124 MB at n = 630, N = 1024); a second call is a no-op.  sk must be the
- * secret key the eval key was made from (checked against a digest of the
- * eval key's public key-switching key: TFHE_EINVAL otherwise). */
+ * (124 MB at n = 630, N = 1024), and for N <= 1024 the same entries in the
+ * transform domain, split into two 16-bit parts, that the key switch runs
+ * on: n * ks_t * (2^ks_basebit - 1) * 4 * N/2 complex doubles (495 MB at
+ * n = 630, N = 1024).  A second call is a no-op.  sk must be the secret key
+ * the eval key was made from (checked against a digest of the eval key's
+ * public key-switching key: TFHE_EINVAL otherwise). */
 int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek);
 
 /* Client side: copy the packing key (built on first use) to host memory,
@@ -292,6 +295,9 @@ int tfhe_export_packing_key(tfhe_secret_key* sk, uint32_t* pks);
  * [B][Z][n+1] device, Z <= N samples per output under s; out: [B][2][N]
  * device, TRLWE samples (A, B) under S whose phase is sum_z phase_z X^z up to
  * the rounding of each a_{z,i} to ks_t * ks_basebit bits and the key noise.
+ * The result is exact mod 2^32: for N <= 1024 the sum of key entries rotated
+ * by X^z is computed as products of 0/1 polynomials by the key entries on
+ * the transform, whose worst-case error stays below 1/8 before rounding.
  * Needs the packing key (tfhe_packing_key_upload), ks_t * ks_basebit <= 16
  * and ks_basebit <= 2.  out must not alias lwe. */
 int tfhe_pack_keyswitch_batch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out,

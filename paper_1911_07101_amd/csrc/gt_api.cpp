@@ -264,6 +264,9 @@ int tfhe_eval_key_upload(const tfhe_secret_key* sk, int device, tfhe_eval_key** 
   ek->ksk_mfma = nullptr;
   ek->pks = nullptr;
   ek->pks_bytes = 0;
+  ek->pks_fft = nullptr;
+  ek->pks_fft_bytes = 0;
+  ek->pks_ic_max = 0;
   ek->key_tag = key_tag(*sk);
   // [n][2l][2 * parts][N/2] complex doubles
   ek->bk_bytes = static_cast<int64_t>(p.n) * 2 * p.l * 2 * ek->parts * (p.N / 2) * 16;
@@ -353,6 +356,7 @@ void tfhe_eval_key_free(tfhe_eval_key* ek) {
   if (ek->ksk) (void)hipFree(ek->ksk);
   if (ek->ksk_mfma) (void)hipFree(ek->ksk_mfma);
   if (ek->pks) (void)hipFree(ek->pks);
+  if (ek->pks_fft) (void)hipFree(ek->pks_fft);
   delete ek;
 }
 
@@ -385,18 +389,57 @@ int tfhe_packing_key_upload(tfhe_secret_key* sk, tfhe_eval_key* ek) {
   } catch (const std::bad_alloc&) {
     return fail(TFHE_ENOMEM, "host allocation failed for the packing key");
   }
+  // For N <= 1024 the key switch runs on the transform (pack_ks_fft_kernel):
+  // each entry is a product of a 0/1 polynomial by a key polynomial split
+  // into two 16-bit parts, and the products of up to ic_max input
+  // coefficients (t (base - 1) entries each) are summed before one rounding,
+  // ic_max the largest count (at most 64) whose worst-case error stays
+  // below 1/8.
+  const tfhe_params& p = ek->p;
+  const int vals = (1 << p.ks_basebit) - 1;
+  const int64_t rows = static_cast<int64_t>(p.n) * p.ks_t * vals;
+  int ic_max = 0;
+  if (p.N <= 1024 && p.ks_t * p.ks_basebit <= 16 && vals <= 3)
+    while (ic_max < 64 && ic_max < p.n &&
+           transform_error_bound_rows(p.N, 2, static_cast<double>(ic_max + 1) * p.ks_t * vals, 1.0) <= 0.125)
+      ic_max++;
+  std::vector<double> fft_host;
+  try {
+    if (ic_max > 0) {
+      fft_host.resize(static_cast<size_t>(rows) * 2 * 2 * p.N);
+      trlwe_rows_to_transform_host(p.N, 2, rows, sk->pks.data(), fft_host.data());
+    }
+  } catch (const std::bad_alloc&) {
+    return fail(TFHE_ENOMEM, "host allocation failed for the packing key's transform");
+  }
   DeviceGuard g(ek->device);
   if (!g.ok) return fail(TFHE_EDEVICE, "cannot select device %d", ek->device);
   const int64_t bytes = static_cast<int64_t>(sk->pks.size()) * 4;
+  const int64_t fft_bytes = static_cast<int64_t>(fft_host.size()) * 8;
   uint32_t* d = nullptr;
+  double* df = nullptr;
   hipError_t e;
   if ((e = hipMalloc(&d, bytes)) != hipSuccess) return fail(TFHE_ENOMEM, "hipMalloc(pks): %s", hipGetErrorString(e));
   if ((e = hipMemcpy(d, sk->pks.data(), bytes, hipMemcpyHostToDevice)) != hipSuccess) {
     (void)hipFree(d);
     return hip_fail(e, "copy pks");
   }
+  if (fft_bytes > 0) {
+    if ((e = hipMalloc(&df, fft_bytes)) != hipSuccess) {
+      (void)hipFree(d);
+      return fail(TFHE_ENOMEM, "hipMalloc(pks transform): %s", hipGetErrorString(e));
+    }
+    if ((e = hipMemcpy(df, fft_host.data(), fft_bytes, hipMemcpyHostToDevice)) != hipSuccess) {
+      (void)hipFree(d);
+      (void)hipFree(df);
+      return hip_fail(e, "copy pks transform");
+    }
+  }
   ek->pks = d;
   ek->pks_bytes = bytes;
+  ek->pks_fft = df;
+  ek->pks_fft_bytes = fft_bytes;
+  ek->pks_ic_max = df ? ic_max : 0;
   return TFHE_OK;
 }
 

@@ -288,7 +288,7 @@ void split_coefficient(int32_t v, int parts, int64_t* piece) {
 }
 
 struct BkCtx {
-  const tfhe_params* p;
+  int N;
   int parts;
   const uint32_t* bk;
   double* out;
@@ -297,13 +297,13 @@ struct BkCtx {
 
 void bk_convert_rows(int64_t begin, int64_t end, void* vctx) {
   const BkCtx& c = *static_cast<BkCtx*>(vctx);
-  const int N = c.p->N, n = N / 2;
+  const int N = c.N, n = N / 2;
   const int S = c.parts;
   const int loge = ring_log_e(S);
   const int E = 1 << loge, T = n >> loge;
   std::vector<std::vector<ComplexL>> z(S, std::vector<ComplexL>(n));
   int64_t piece_lo[4], piece_hi[4];
-  for (int64_t row = begin; row < end; row++) {  // row = (i * 2l + r) * 2 + q
+  for (int64_t row = begin; row < end; row++) {  // row = (TRLWE row) * 2 + q
     const uint32_t* src = c.bk + row * N;
     for (int j = 0; j < n; j++) {
       split_coefficient(static_cast<int32_t>(src[j]), S, piece_lo);
@@ -334,7 +334,8 @@ int key_part_shift(int parts) { return parts == 2 ? 16 : 11; }
 int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
 
 // Worst-case error of one output coefficient of z = sum_{r<R} x_r * y_r
-// (R = 2l; x_r the digits, |x| <= D = Bg/2; y_r one key part, |y| <= Y = 2^b)
+// (x_r the digits, |x| <= D; y_r one key part, |y| <= Y = 2^b; in the
+// external product R = 2l and D = Bg/2)
 // computed as the library does: X_r = fl(F x_r) on the device, K_r = the
 // key's transform F y_r / n computed in long double and rounded once,
 // P = fl(sum_r X_r K_r) pointwise, z^ = fl(G P) with G the unscaled inverse.
@@ -358,23 +359,25 @@ int key_part_bits(int parts) { return parts == 2 ? 15 : 10; }
 // directions) have a per-stage relative error of at most mu + 3.02u to first
 // order, below the theorem's eta, so eta covers them; the twist is one
 // complex product per point, also within eta.
-double transform_error_bound(const tfhe_params& p, int parts) {
+double transform_error_bound_rows(int ring_n, int parts, double R, double D) {
   const double u = std::ldexp(1.0, -53), u2 = 2 * u;
-  const int n = p.N / 2;
+  const int n = ring_n / 2;
   const double m = ilog2(n);
   const double gamma4 = 4 * u / (1 - 4 * u);
   const double eta = u + gamma4 * (std::sqrt(2.0) + u);
   const double eps = m * eta / (1 - m * eta);
   const double eps_inv = (m + 1) * eta / (1 - (m + 1) * eta);
-  const double R = 2.0 * p.l;
   const double g2R = 2 * R * u / (1 - 2 * R * u);
-  const double D = std::ldexp(1.0, p.bg_bit - 1);
   const double Y = std::ldexp(1.0, key_part_bits(parts));
-  const double N = p.N, sN = std::sqrt(N);
+  const double N = ring_n, sN = std::sqrt(N);
   const double x1 = D * N, x2 = D * sN, y2 = Y * sN;
   const double z2 = R * x1 * y2;
   const double ep = R * (eps * (1 + u2) + u2 + g2R * (1 + eps) * (1 + u2)) * x2 * y2;
   return eps_inv * (z2 + std::sqrt(static_cast<double>(n)) * ep) + ep;
+}
+
+double transform_error_bound(const tfhe_params& p, int parts) {
+  return transform_error_bound_rows(p.N, parts, 2.0 * p.l, std::ldexp(1.0, p.bg_bit - 1));
 }
 
 int key_parts(const tfhe_params& p) {
@@ -383,10 +386,14 @@ int key_parts(const tfhe_params& p) {
   return 0;
 }
 
+void trlwe_rows_to_transform_host(int N, int parts, int64_t rows, const uint32_t* src, double* out) {
+  const std::vector<ComplexL> tw = twiddles_long(N);
+  BkCtx ctx{N, parts, src, out, &tw};
+  parallel_for(rows * 2, 16, bk_convert_rows, &ctx);
+}
+
 void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out) {
-  const std::vector<ComplexL> tw = twiddles_long(p.N);
-  BkCtx ctx{&p, parts, bk, out, &tw};
-  parallel_for(static_cast<int64_t>(p.n) * 2 * p.l * 2, 16, bk_convert_rows, &ctx);
+  trlwe_rows_to_transform_host(p.N, parts, static_cast<int64_t>(p.n) * 2 * p.l, bk, out);
 }
 
 bool ks_uses_mfma(const tfhe_params& p) { return p.ks_t == 8 && p.ks_basebit == 2; }

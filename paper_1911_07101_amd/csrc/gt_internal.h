@@ -28,9 +28,13 @@ struct tfhe_eval_key {
                     // order (ksk_mfma_host), else NULL
   int64_t ksk_mfma_bytes;
   uint32_t* pks;    // device packing key [n][t][base-1][2][N], or NULL until uploaded
+  double* pks_fft;  // the packing key in the transform layout with two parts,
+                    // [n][t (base-1)][4][N/2] complex, for N <= 1024 (else NULL)
+  int pks_ic_max;   // input coefficients whose products may be summed before one rounding
   int64_t bk_bytes;
   int64_t ksk_bytes;
   int64_t pks_bytes;
+  int64_t pks_fft_bytes;
   uint64_t key_tag;  // digest of the start of the key-switching key (public material), which ties
                      // a packing key to the secret key this eval key was made from
 };
@@ -60,8 +64,14 @@ void encrypt_host(const tfhe_secret_key& sk, uint64_t seed, const uint32_t* mu, 
                   int64_t count, uint32_t* ct);
 int key_part_shift(int parts);
 int key_part_bits(int parts);
+// worst-case error of a sum of R products of digits |x| <= D by key parts
+// at ring degree N (the external product: R = 2l, D = Bg/2)
+double transform_error_bound_rows(int N, int parts, double R, double D);
 double transform_error_bound(const tfhe_params& p, int parts);
 int key_parts(const tfhe_params& p);  // 2 or 3, 0 if no split keeps the bound
+// TRLWE samples [rows][2][N] (u32) to the transform layout of the
+// bootstrapping key: [rows][2 parts][N/2] complex, output slot q * parts + s
+void trlwe_rows_to_transform_host(int N, int parts, int64_t rows, const uint32_t* src, double* out);
 void bk_to_transform_host(const tfhe_params& p, int parts, const uint32_t* bk, double* out);
 
 // Key switching with t = 8 digits of 2 bits runs on the matrix cores: the

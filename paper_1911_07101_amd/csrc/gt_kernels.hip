@@ -15,8 +15,9 @@
 //   relu_sign_kernel       trivial 0 for the sign bit of the ReLU output
 //   cmux_abar_kernel       modulus-switched inputs of a one-CMux stage check
 //   not_kernel             NOT without bootstrapping
-//   pack_init_kernel, pack_ks_kernel  functional key switching of LWE samples
-//                          into one ring sample
+//   pack_init_kernel, pack_ks_fft_kernel, pack_ks_kernel  functional key
+//                          switching of LWE samples into one ring sample (on
+//                          the transform for N <= 1024, else directly)
 //   sample_extract_kernel  LWE samples of chosen coefficients of ring samples
 //   negacyclic_mul_kernel  standalone ring product (checks the transform)
 //
@@ -1572,6 +1573,143 @@ __global__ __launch_bounds__(256) void pack_ks_kernel(const uint32_t* __restrict
   for (int w = 0; w < W; w++) atomicAdd(out + b * 2 * N + threadIdx.x + 256 * w, acc[w]);
 }
 
+// The same on the transform (N <= 1024): sum_{z,i,j} X^z PKS[i][j][v_{z,i,j}]
+// = sum_{i,j,v} M_{i,j,v} PKS[i][j][v], M_{i,j,v} = sum of X^z over the
+// samples z whose digit j of the rounded a_{z,i} is v: one negacyclic
+// product of a 0/1 polynomial by each key entry, computed as in the external
+// product (the entry in the transform domain in two 16-bit parts, the
+// products summed there, one inverse transform and one rounding per block,
+// exact because the sum's worst-case error stays below 1/8 for up to
+// pks_ic_max input coefficients).  A block takes IC input coefficients of
+// CPB TRLWE outputs, one per T lanes; its waves read the same key entries
+// close together in time, which L1 then serves; each adds its exact partial
+// sum to out with 32-bit atomics after pack_init_kernel.  Workgroups are
+// remapped so that the blocks of one coefficient range run on one XCD (its
+// L2 then holds the range's key entries for all of them).
+template <int LOGN, int WPB>
+__global__ __launch_bounds__((BrCfg<LOGN, 2, WPB>::THREADS), (BrCfg<LOGN, 2, WPB>::MIN_WAVES)) void pack_ks_fft_kernel(
+    const double2* __restrict__ pkf, const double2* __restrict__ tw_g, const uint32_t* __restrict__ lwe, int n,
+    int Z, int t_digits, int basebit, int IC, int groups, int64_t B, uint32_t* __restrict__ out) {
+  using C = BrCfg<LOGN, 2, WPB>;
+  using Lay = typename C::Lay;
+  constexpr int NR = C::NR, NC = C::NC, E = C::E, T = C::T, CPB = C::CPB, O = C::O;
+  if constexpr (C::MIN_WAVES == 1) asm volatile("" ::: "a255");
+  __shared__ double2 s_tw[NC];
+  __shared__ double2 s_scr[CPB * Lay::SCR];
+  __shared__ double2 s_itw[C::ITW_LDS ? NC - 1 : 1];
+
+  const unsigned G = gridDim.x, xcd = blockIdx.x % 8u, q8 = G / 8u, r8 = G % 8u;
+  const unsigned L = xcd * q8 + min(xcd, r8) + blockIdx.x / 8u;
+  const int grp = static_cast<int>(L % static_cast<unsigned>(groups));
+  const int i0 = static_cast<int>(L / static_cast<unsigned>(groups)) * IC;
+  const int i1 = min(n, i0 + IC);
+  const int slot = threadIdx.x / T;
+  const int t = threadIdx.x % T;
+  int64_t b = static_cast<int64_t>(grp) * CPB + slot;
+  const bool active = b < B;
+  if (!active) b = B - 1;  // idle slots repeat the last output and write nothing
+
+  for (int k = threadIdx.x; k < NC; k += C::THREADS) s_tw[tw_lds_slot<Lay>(k)] = tw_g[k];
+  if constexpr (C::ITW_LDS)
+    for (int k = threadIdx.x; k < NC - 1; k += C::THREADS) s_itw[k] = tw_g[NC + k];
+  const auto itw = [&] {
+    if constexpr (C::ITW_LDS)
+      return PtrTable{s_itw};
+    else
+      return BufTable{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + NC), 0, NC * 16, 0x00020000)};
+  }();
+  const BufTable twist{__builtin_amdgcn_make_buffer_rsrc(const_cast<double2*>(tw_g + 2 * NC), 0, NC * 16, 0x00020000)};
+  __syncthreads();
+  double2* scr = s_scr + slot * Lay::SCR;
+
+  const int vals = (1 << basebit) - 1, R = t_digits * vals, prec = t_digits * basebit;
+  const uint32_t round = 1u << (31 - prec);  // prec <= 16
+  // this output's Z input samples through a buffer resource: an offset past
+  // the last sample (z >= Z) reads 0, which rounds to 0 and matches no digit v >= 1
+  const __amdgpu_buffer_rsrc_t lr = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(lwe + b * Z * (n + 1)), 0, Z * (n + 1) * 4, 0x00020000);
+  const size_t key_step = static_cast<size_t>(R) * O * NC;  // points per input coefficient
+  const uint32_t voff = static_cast<uint32_t>(t) * 16u;
+  double2 acc[O][E];
+#pragma unroll
+  for (int o = 0; o < O; o++)
+#pragma unroll
+    for (int e = 0; e < E; e++) acc[o][e] = make_double2(0.0, 0.0);
+
+  for (int i = i0; i < i1; i++) {
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<double2*>(pkf + static_cast<size_t>(i) * key_step), 0, static_cast<int>(key_step * 16), 0x00020000);
+    // rounded a_{z,i} at this lane's coefficients z = t + T e (real part of
+    // point e) and z + N/2 (imaginary part); the lane's offset is recomputed
+    // here (the empty asm hides t) rather than kept live across the loop
+    int t_q = t;
+    asm volatile("" : "+v"(t_q));
+    const uint32_t lane_off = static_cast<uint32_t>((t_q * (n + 1) + i) * 4);
+    uint32_t r[2][E];
+#pragma unroll
+    for (int e = 0; e < E; e++)
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const uint32_t z_off = static_cast<uint32_t>((T * e + h * NC) * (n + 1) * 4);
+        const uint32_t a = static_cast<uint32_t>(__builtin_amdgcn_raw_buffer_load_b32(lr, lane_off, z_off, 0));
+        r[h][e] = (a + round) >> (32 - prec);
+      }
+    for (int j = 0; j < t_digits; j++) {
+      const uint32_t sh = static_cast<uint32_t>((t_digits - 1 - j) * basebit);
+      for (int v = 1; v <= vals; v++) {
+        const uint32_t row = static_cast<uint32_t>((j * vals + v - 1) * O * NC) * 16u;
+        // one-wave blocks (the whole register file) request the first
+        // output's key points before the transform; two waves per SIMD have
+        // no registers for them there
+        double2 w[E];
+        if constexpr (C::MIN_WAVES == 1) {
+#pragma unroll
+          for (int e = 0; e < E; e++) w[e] = load_b128(kr, voff, row + static_cast<uint32_t>(e * T * 16));
+        }
+        double2 x[E];
+#pragma unroll
+        for (int e = 0; e < E; e++)
+          x[e] = make_double2(((r[0][e] >> sh) & static_cast<uint32_t>(vals)) == static_cast<uint32_t>(v) ? 1.0 : 0.0,
+                              ((r[1][e] >> sh) & static_cast<uint32_t>(vals)) == static_cast<uint32_t>(v) ? 1.0 : 0.0);
+        fft_forward<Lay, true>(x, t, scr, s_tw, tw_g, 1);
+#pragma unroll
+        for (int o = 0; o < O; o++) {
+          if (o > 0 || C::MIN_WAVES != 1) {
+#pragma unroll
+            for (int e = 0; e < E; e++) w[e] = load_b128(kr, voff, row + static_cast<uint32_t>((o * E + e) * T * 16));
+          }
+#pragma unroll
+          for (int e = 0; e < E; e++) cmac(acc[o][e], x[e], w[e]);
+        }
+      }
+    }
+  }
+
+  static_for<0, O / 2>([&](auto PI) { fft_inverse<Lay, 2 * decltype(PI)::value, 2>(acc, t, scr, itw); });
+  if (!active) return;
+  uint32_t* dst = out + b * 2 * NR;
+  int t_r = t;
+  asm volatile("" : "+v"(t_r));
+#pragma unroll
+  for (int e = 0; e < E; e++) {
+    const int j = t_r + T * e;
+    const double2 tau = twist(t_r, T * e);
+    uint32_t ra0 = 0u, ra1 = 0u, rb0 = 0u, rb1 = 0u;
+#pragma unroll
+    for (int sp = 1; sp >= 0; sp--) {
+      const double2 va = cmul(acc[sp][e], tau), vb = cmul(acc[2 + sp][e], tau);
+      ra0 = (ra0 << 16) + round_low32(va.x);
+      ra1 = (ra1 << 16) + round_low32(va.y);
+      rb0 = (rb0 << 16) + round_low32(vb.x);
+      rb1 = (rb1 << 16) + round_low32(vb.y);
+    }
+    atomicAdd(dst + j, 0u - ra0);
+    atomicAdd(dst + j + NC, 0u - ra1);
+    atomicAdd(dst + NR + j, 0u - rb0);
+    atomicAdd(dst + NR + j + NC, 0u - rb1);
+  }
+}
+
 // SampleExtract of coefficients 0 .. K-1 (Section 3.2, step 3): out[b][i] =
 // (a'_0 .. a'_{N-1}, B_i), a'_j = A_{i-j} (j <= i) or -A_{N+i-j} (j > i)
 __global__ __launch_bounds__(256) void sample_extract_kernel(const uint32_t* __restrict__ trlwe, int N, int64_t B,
@@ -1906,6 +2044,45 @@ int launch_lut_leaf(const tfhe_eval_key* ek, const uint32_t* x, int32_t msg_bits
   return launch_status("lut_leaf_kernel");
 }
 
+// The packing key switch on the transform: at N = 1024 blocks of 8 waves when
+// the batch fills one (their outputs share the key reads in L1), else
+// one-wave blocks;
+// IC input coefficients per block, at most pks_ic_max, chosen so that the
+// rounds of resident blocks times a block's work (IC t (base - 1) forward
+// transforms and four inverse ones) is least.
+template <int WPB, int LOGN>
+int launch_pack_fft_blocks(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
+                           hipStream_t st) {
+  using C = BrCfg<LOGN, 2, WPB>;
+  const tfhe_params& p = ek->p;
+  const int vals = (1 << p.ks_basebit) - 1, R = p.ks_t * vals;
+  const int64_t cus = ek->cus > 0 ? ek->cus : 256;
+  const int64_t groups = (B + C::CPB - 1) / C::CPB;
+  const int64_t resident = cus * (WPB == 8 ? 1 : 4);
+  int64_t best_ic = 1, best = -1;
+  for (int64_t ic = 1; ic <= ek->pks_ic_max; ic++) {
+    const int64_t blocks = groups * ((p.n + ic - 1) / ic);
+    const int64_t cost = (blocks + resident - 1) / resident * (ic * R + 4);
+    if (best < 0 || cost < best) best = cost, best_ic = ic;
+  }
+  const int64_t blocks = groups * ((p.n + best_ic - 1) / best_ic);
+  if (blocks > 0x7fffffff) return fail(TFHE_EINVAL, "too many TRLWE outputs for one launch");
+  hipLaunchKernelGGL((pack_ks_fft_kernel<LOGN, WPB>), dim3(static_cast<unsigned>(blocks)), dim3(C::THREADS), 0, st,
+                     reinterpret_cast<const double2*>(ek->pks_fft), reinterpret_cast<const double2*>(ek->tw), lwe,
+                     p.n, Z, p.ks_t, p.ks_basebit, static_cast<int>(best_ic), static_cast<int>(groups), B, out);
+  return launch_status("pack_ks_fft_kernel");
+}
+
+template <int LOGN>
+int launch_pack_fft(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
+                    hipStream_t st) {
+  // (blocks of 8 waves at N < 1024 would spill registers: one-wave blocks
+  // there hold 64 / T outputs each)
+  if constexpr (LOGN == 10)
+    if (B >= 8) return launch_pack_fft_blocks<8, LOGN>(ek, lwe, Z, out, B, st);
+  return launch_pack_fft_blocks<1, LOGN>(ek, lwe, Z, out, B, st);
+}
+
 int launch_pack_keyswitch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t Z, uint32_t* out, int64_t B,
                           void* stream) {
   const tfhe_params& p = ek->p;
@@ -1917,6 +2094,14 @@ int launch_pack_keyswitch(const tfhe_eval_key* ek, const uint32_t* lwe, int32_t 
                      p.n, p.N, Z, B, out);
   int rc = launch_status("pack_init_kernel");
   if (rc) return rc;
+  if (ek->pks_fft != nullptr) {
+    switch (p.N) {
+      case 256: return launch_pack_fft<8>(ek, lwe, Z, out, B, st);
+      case 512: return launch_pack_fft<9>(ek, lwe, Z, out, B, st);
+      case 1024: return launch_pack_fft<10>(ek, lwe, Z, out, B, st);
+      default: break;
+    }
+  }
   dim3 grid(static_cast<unsigned>(B), static_cast<unsigned>((p.n + PKS_IC - 1) / PKS_IC));
   switch (p.N) {
     case 256: hipLaunchKernelGGL(pack_ks_kernel<256>, grid, dim3(256), 0, st, lwe, ek->pks, p.n, Z, p.ks_t, p.ks_basebit, out); break;

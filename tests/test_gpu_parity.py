@@ -622,6 +622,44 @@ def test_pack_keyswitch_toy(torch):
             assert np.array_equal(((ph + (1 << 25)) >> 26) % 64, m[b])
 
 
+
+@pytest.mark.parametrize("B,Z,check", [(9, 1000, (0, 8)), (3, 517, (2,))])
+def test_pack_keyswitch_transform_128bit(torch, B, Z, check):
+    """Packing key switching at the 128-bit parameters on the transform
+    path: nine outputs (a block of eight and a ragged block of one) and three
+    outputs in one-wave blocks, Z samples each; the checked outputs bit-exact
+    with the oracle, and every coefficient z of every output decodes to
+    message z."""
+    p = wl.CONFIGS["tfhe128_nand"]["params"]
+    sk, ek, ok = keys_for("tfhe128_nand", torch)
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    m = np.random.default_rng(70 + B).integers(0, 16, (B, Z)).astype(np.uint32)
+    lwe = tfhe.tfhe_encrypt_torus(sk, 70 + B, (m.ravel() << 28).astype(np.uint32)).reshape(B, Z, p["n"] + 1)
+    say(f"pack keyswitch 128-bit B={B} Z={Z}")
+    got = tfhe.tfhe_pack_keyswitch_batch(ek, tfhe.to_device(lwe))
+    ext = tfhe.to_host(tfhe.tfhe_sample_extract_batch(got, Z))
+    ph = tfhe.tfhe_decrypt_phase(sk, ext, key_kind=1).astype(np.int64)
+    assert np.array_equal(((ph + (1 << 27)) >> 28) % 16, m)
+    got = tfhe.to_host(got)
+    for b in check:
+        assert np.array_equal(got[b], oracle.pack_keyswitch(ok, lwe[b])), b
+
+
+def test_pack_keyswitch_n2048(torch):
+    """Packing key switching at N = 2048 (n = 750), which takes the
+    coefficient-domain kernel: two outputs of 37 samples, bit-exact with the
+    oracle."""
+    p = wl.CONFIGS["lut3_n2048"]["params"]
+    sk, ek, ok = keys_for("lut3_n2048", torch)
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    B, Z = 2, 37
+    m = np.random.default_rng(73).integers(0, 16, (B, Z)).astype(np.uint32)
+    lwe = tfhe.tfhe_encrypt_torus(sk, 73, (m.ravel() << 28).astype(np.uint32)).reshape(B, Z, p["n"] + 1)
+    say(f"pack keyswitch n=750 N=2048 B={B} Z={Z}")
+    got = tfhe.to_host(tfhe.tfhe_pack_keyswitch_batch(ek, tfhe.to_device(lwe)))
+    for b in range(B):
+        assert np.array_equal(got[b], oracle.pack_keyswitch(ok, lwe[b])), b
+
 def test_sample_extract_batch(torch):
     """SampleExtract of the first K coefficients of random TRLWE samples
     equals the oracle's extraction of each coefficient."""
