@@ -340,35 +340,37 @@ def suite(path: str):
          unit="gate bootstraps/s", ok=bool(ok))
     del u, d, y, ws
 
-    # TFHE side of the BGV-to-TFHE switch for the MLP layer's 7680 values:
-    # LWE samples (n = 630) of 4-bit messages packed 960 to a TRLWE sample
-    # (step 2), the 960 coefficients of each extracted (step 3) and
-    # key-switched back to n; every value decodes to its message.  Step 4
-    # (TFHE to BGV) is a programmable bootstrap with a torus test vector:
-    # the LUT bootstrap measured last.
-    cfg = wl.CONFIGS["mlp_relu"]
-    V, Zp, seed = cfg["values"], 960, cfg["input_seed"] + 5
-    msgs = wl.messages(seed, V, 4)
-    lwe = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, seed, (msgs << 28).astype(np.uint32))
-                         .reshape(V // Zp, Zp, p["n"] + 1))
+    # TFHE side of the BGV-to-TFHE switch for the MLP layer's 7680 values and
+    # the conv layer's 207,360: LWE samples (n = 630) of 4-bit messages packed
+    # 960 to a TRLWE sample (step 2), the 960 coefficients of each extracted
+    # (step 3) and key-switched back to n; every value decodes to its
+    # message.  Step 4 (TFHE to BGV) is a programmable bootstrap with a torus
+    # test vector: the LUT bootstrap measured last.
     t0 = time.perf_counter()
     tfhe.tfhe_packing_key_upload(sk, ek)
     pk_s = time.perf_counter() - t0
-    packed = torch.empty((V // Zp, 2, p["N"]), dtype=torch.int32, device=dev)
-    ext = torch.empty((V // Zp, Zp, p["N"] + 1), dtype=torch.int32, device=dev)
-    back = torch.empty((V, p["n"] + 1), dtype=torch.int32, device=dev)
-    steps = [lambda: tfhe.tfhe_pack_keyswitch_batch(ek, lwe, out=packed, stream=stream),
-             lambda: tfhe.tfhe_sample_extract_batch(packed, Zp, out=ext, stream=stream),
-             lambda: tfhe.tfhe_keyswitch_batch(ek, ext.view(V, p["N"] + 1), out=back, stream=stream)]
-    for f in steps:
-        f()
-    step_ms = [_timed(f, 5) for f in steps]
-    ph = tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(back)).astype(np.int64)
-    ok = np.array_equal(((ph + (1 << 27)) >> 28) % 16, msgs)
-    emit(workload="switch_bgv_to_tfhe", values=V, lwe_per_trlwe=Zp, pack_keyswitch_ms=step_ms[0],
-         sample_extract_ms=step_ms[1], keyswitch_ms=step_ms[2], per_s=V / sum(step_ms) * 1e3,
-         unit="values/s", packing_key_build_s=pk_s, ok=bool(ok))
-    del lwe, packed, ext, back
+    Zp = 960
+    for layer in ("mlp_relu", "conv_relu"):
+        cfg = wl.CONFIGS[layer]
+        V, seed = cfg["values"], cfg["input_seed"] + 5
+        msgs = wl.messages(seed, V, 4)
+        lwe = tfhe.to_device(tfhe.tfhe_encrypt_torus(sk, seed, (msgs << 28).astype(np.uint32))
+                             .reshape(V // Zp, Zp, p["n"] + 1))
+        packed = torch.empty((V // Zp, 2, p["N"]), dtype=torch.int32, device=dev)
+        ext = torch.empty((V // Zp, Zp, p["N"] + 1), dtype=torch.int32, device=dev)
+        back = torch.empty((V, p["n"] + 1), dtype=torch.int32, device=dev)
+        steps = [lambda: tfhe.tfhe_pack_keyswitch_batch(ek, lwe, out=packed, stream=stream),
+                 lambda: tfhe.tfhe_sample_extract_batch(packed, Zp, out=ext, stream=stream),
+                 lambda: tfhe.tfhe_keyswitch_batch(ek, ext.view(V, p["N"] + 1), out=back, stream=stream)]
+        for f in steps:
+            f()
+        step_ms = [_timed(f, 5) for f in steps]
+        ph = tfhe.tfhe_decrypt_phase(sk, tfhe.to_host(back)).astype(np.int64)
+        ok = np.array_equal(((ph + (1 << 27)) >> 28) % 16, msgs)
+        emit(workload="switch_bgv_to_tfhe", layer=layer, values=V, lwe_per_trlwe=Zp,
+             pack_keyswitch_ms=step_ms[0], sample_extract_ms=step_ms[1], keyswitch_ms=step_ms[2],
+             per_s=V / sum(step_ms) * 1e3, unit="values/s", packing_key_build_s=pk_s, ok=bool(ok))
+        del lwe, packed, ext, back
 
     # conv ReLU: 207,360 values, calls of 16,384 gates; inputs resident in HBM
     cfg = wl.CONFIGS["conv_relu"]
