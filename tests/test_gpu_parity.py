@@ -645,6 +645,24 @@ def test_pack_keyswitch_transform_128bit(torch, B, Z, check):
         assert np.array_equal(got[b], oracle.pack_keyswitch(ok, lwe[b])), b
 
 
+
+@pytest.mark.parametrize("N,ks_t,ks_basebit,B,Z", [(512, 4, 2, 5, 300), (1024, 12, 1, 9, 77)])
+def test_pack_keyswitch_transform_shapes(torch, N, ks_t, ks_basebit, B, Z):
+    """The transform path of the packing key switch at other ring sizes and
+    digit shapes: one-wave blocks of two outputs at N = 512 with base-4
+    digits, and blocks of eight outputs at N = 1024 with base-2 digits (one
+    key entry per digit), ragged batches, every output bit-exact with the
+    oracle."""
+    p = dict(wl.CONFIGS["toy"]["params"], n=40, N=N, ks_t=ks_t, ks_basebit=ks_basebit)
+    sk, ek, ok = keys_for(f"pack{N}t{ks_t}b{ks_basebit}", torch, p, 0x9A00 + N + ks_t)
+    tfhe.tfhe_packing_key_upload(sk, ek)
+    m = np.random.default_rng(N + ks_t).integers(0, 16, (B, Z)).astype(np.uint32)
+    lwe = tfhe.tfhe_encrypt_torus(sk, 80 + ks_t, (m.ravel() << 28).astype(np.uint32)).reshape(B, Z, p["n"] + 1)
+    say(f"pack keyswitch N={N} t={ks_t} basebit={ks_basebit} B={B} Z={Z}")
+    got = tfhe.to_host(tfhe.tfhe_pack_keyswitch_batch(ek, tfhe.to_device(lwe)))
+    for b in range(B):
+        assert np.array_equal(got[b], oracle.pack_keyswitch(ok, lwe[b])), b
+
 def test_pack_keyswitch_n2048(torch):
     """Packing key switching at N = 2048 (n = 750), which takes the
     coefficient-domain kernel: two outputs of 37 samples, bit-exact with the
